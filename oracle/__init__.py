@@ -1,0 +1,13 @@
+"""CPU fp64 oracle for the SiLU Gated MLP (test infrastructure only).
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the HIP path.
+"""
+from .oracle import (  # noqa: F401
+    Oracle,
+    build,
+    default_oracle,
+    gated_mlp_rows,
+    silu,
+)
+from .brute import brute_gated_mlp, brute_silu  # noqa: F401

@@ -1,0 +1,211 @@
+/*
+ * CPU fp64 oracle for the SiLU Gated MLP  Y = (silu(X Wg) * (X Wu)) Wd.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
+ * call this file: only the test-suite, the smoke check and the CPU-baseline
+ * leg of the benchmark use it.  It shares no code, header, table or helper
+ * with the HIP library.
+ *
+ * What it computes is the plain definition, written out:
+ *   - the Gated MLP graph of the paper's Fig. "Gated MLP" (fig:mlp-example,
+ *     Section 4.1): X feeds two matmuls (W1 -> silu, W2), their results are
+ *     multiplied elementwise, and the product feeds a third matmul with W3.
+ *     Here W1 = Wg (gate), W2 = Wu (up), W3 = Wd (down).
+ *   - matmul(a, b)[i, j] = sum over k of a[i, k] * b[k, j]  (matmul semantics,
+ *     Fig. fig:op-sema in Section 4.2.1, and the granular-operation table
+ *     tab:nki-ops in Section 5.1).
+ *   - silu(x) = x * sigmoid(x)  (granular-operation table tab:nki-ops).
+ *
+ * Every step is done in IEEE double precision (no fused multiply-add: the
+ * build passes -ffp-contract=off).  bf16 inputs are decoded exactly (a bf16
+ * is the top 16 bits of an IEEE binary32), so the oracle sees exactly the
+ * values the GPU sees.  Each output element is accumulated in ascending
+ * index order; the loop over output columns is only placed inside the
+ * reduction loop for memory order, which leaves every element's own
+ * accumulation order unchanged.
+ *
+ * Rows of X are independent, so the entry points take a list of rows and
+ * compute only those (this lets large shapes be checked on sampled rows).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* silu(z) = z * sigmoid(z) = z / (1 + exp(-z)).  For z < 0 the algebraically
+ * equal form z * exp(z) / (1 + exp(z)) is used so that exp never overflows. */
+double gmlp_oracle_silu(double z)
+{
+    if (z >= 0.0)
+        return z / (1.0 + exp(-z));
+    double e = exp(z);
+    return z * e / (1.0 + e);
+}
+
+/* Exact bf16 -> double: the 16 bits are the high half of a binary32. */
+double gmlp_oracle_bf16_to_f64(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static inline double ld_f64(const double *p, int64_t i) { return p[i]; }
+static inline double ld_bf16(const uint16_t *p, int64_t i)
+{
+    uint32_t u = (uint32_t)p[i] << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/*
+ * The two steps of one row, for one element type WT decoded by LD:
+ *
+ *   gate_up: for f in [f_lo, f_hi):
+ *              G[f] = sum_d x[d] Wg[d, f]      (d ascending)
+ *              U[f] = sum_d x[d] Wu[d, f]      (d ascending)
+ *              H[f] = silu(G[f]) * U[f]
+ *   down:    for j in [j_lo, j_hi):
+ *              Y[j] = sum_f H[f] Wd[f, j]      (f ascending)
+ *
+ * The column ranges only split work between threads.
+ */
+#define DEFINE_ROW_STEPS(SUF, WT, LD)                                           \
+    static int gate_up_##SUF(const WT *x, const WT *Wg, const WT *Wu,           \
+                             int64_t D, int64_t F, int64_t f_lo,                \
+                             int64_t f_hi, double *h)                           \
+    {                                                                           \
+        int64_t w = f_hi - f_lo;                                                \
+        double *g = (double *)calloc((size_t)w, sizeof(double));                \
+        double *u = (double *)calloc((size_t)w, sizeof(double));                \
+        if (!g || !u) {                                                         \
+            free(g);                                                            \
+            free(u);                                                            \
+            return 1;                                                           \
+        }                                                                       \
+        for (int64_t d = 0; d < D; ++d) {                                       \
+            double xd = LD(x, d);                                               \
+            for (int64_t j = 0; j < w; ++j) {                                   \
+                g[j] += xd * LD(Wg, d * F + f_lo + j);                          \
+                u[j] += xd * LD(Wu, d * F + f_lo + j);                          \
+            }                                                                   \
+        }                                                                       \
+        for (int64_t j = 0; j < w; ++j)                                         \
+            h[f_lo + j] = gmlp_oracle_silu(g[j]) * u[j];                        \
+        free(g);                                                                \
+        free(u);                                                                \
+        return 0;                                                               \
+    }                                                                           \
+    static void down_##SUF(const double *h, const WT *Wd, int64_t F,            \
+                           int64_t D, int64_t j_lo, int64_t j_hi, double *y)    \
+    {                                                                           \
+        for (int64_t j = j_lo; j < j_hi; ++j)                                   \
+            y[j] = 0.0;                                                         \
+        for (int64_t f = 0; f < F; ++f) {                                       \
+            double hf = h[f];                                                   \
+            for (int64_t j = j_lo; j < j_hi; ++j)                               \
+                y[j] += hf * LD(Wd, f * D + j);                                 \
+        }                                                                       \
+    }
+
+DEFINE_ROW_STEPS(bf16, uint16_t, ld_bf16)
+DEFINE_ROW_STEPS(f64, double, ld_f64)
+
+/* Width of the column ranges handed to threads when few rows are requested. */
+#define CHUNK 256
+
+static int check_args(const void *X, const void *Wg, const void *Wu, const void *Wd,
+                      int64_t T, int64_t D, int64_t F, const int64_t *rows, int64_t n,
+                      const double *Y)
+{
+    if (D <= 0 || F <= 0 || T < 0 || n < 0 || !X || !Wg || !Wu || !Wd || !Y)
+        return 1;
+    for (int64_t r = 0; r < n; ++r) {
+        int64_t t = rows ? rows[r] : r;
+        if (t < 0 || t >= T)
+            return 2;
+    }
+    return 0;
+}
+
+static int pick_threads(int threads)
+{
+    if (threads > 0)
+        return threads;
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/*
+ * Entry points.  Arrays are row-major: X [T, D], Wg [D, F], Wu [D, F],
+ * Wd [F, D].  rows[n] lists the rows of X to evaluate (NULL means rows
+ * 0..n-1).  Outputs: Y [n, D] and, if H is not NULL, H [n, F] (the product
+ * silu(G) * U before the down projection).  threads <= 0 uses the OpenMP
+ * default.  Returns 0 on success, 1 on a bad argument, 2 on a row index
+ * outside [0, T), 3 on allocation failure.
+ */
+#define ORACLE_DRIVER(SUF, WT)                                                  \
+    int rc = check_args(X, Wg, Wu, Wd, T, D, F, rows, n, Y);                    \
+    if (rc)                                                                     \
+        return rc;                                                              \
+    if (n == 0)                                                                 \
+        return 0;                                                               \
+    int nthr = pick_threads(threads);                                           \
+    double *h_all = (double *)malloc(sizeof(double) * (size_t)n * (size_t)F);   \
+    if (!h_all)                                                                 \
+        return 3;                                                               \
+    /* Many rows: one row per task.  Few rows: column ranges per task. */       \
+    int64_t fc = n >= nthr ? F : CHUNK, dc = n >= nthr ? D : CHUNK;             \
+    int64_t nfc = (F + fc - 1) / fc, ndc = (D + dc - 1) / dc;                   \
+    int fail = 0;                                                               \
+    _Pragma("omp parallel for num_threads(nthr) schedule(dynamic, 1) reduction(|:fail)") \
+    for (int64_t task = 0; task < n * nfc; ++task) {                            \
+        int64_t r = task / nfc, f_lo = (task % nfc) * fc;                       \
+        int64_t f_hi = f_lo + fc < F ? f_lo + fc : F;                           \
+        int64_t t = rows ? rows[r] : r;                                         \
+        fail |= gate_up_##SUF(X + t * D, Wg, Wu, D, F, f_lo, f_hi, h_all + r * F); \
+    }                                                                           \
+    if (fail) {                                                                 \
+        free(h_all);                                                            \
+        return 3;                                                               \
+    }                                                                           \
+    _Pragma("omp parallel for num_threads(nthr) schedule(dynamic, 1)")          \
+    for (int64_t task = 0; task < n * ndc; ++task) {                            \
+        int64_t r = task / ndc, j_lo = (task % ndc) * dc;                       \
+        int64_t j_hi = j_lo + dc < D ? j_lo + dc : D;                           \
+        down_##SUF(h_all + r * F, Wd, F, D, j_lo, j_hi, Y + r * D);             \
+    }                                                                           \
+    if (H)                                                                      \
+        memcpy(H, h_all, sizeof(double) * (size_t)n * (size_t)F);               \
+    free(h_all);                                                                \
+    return 0;
+
+int gmlp_oracle_rows_bf16(const uint16_t *X, const uint16_t *Wg, const uint16_t *Wu,
+                          const uint16_t *Wd, int64_t T, int64_t D, int64_t F,
+                          const int64_t *rows, int64_t n, double *Y, double *H,
+                          int threads)
+{
+    ORACLE_DRIVER(bf16, uint16_t)
+}
+
+int gmlp_oracle_rows_f64(const double *X, const double *Wg, const double *Wu,
+                         const double *Wd, int64_t T, int64_t D, int64_t F,
+                         const int64_t *rows, int64_t n, double *Y, double *H,
+                         int threads)
+{
+    ORACLE_DRIVER(f64, double)
+}
+
+/* Number of threads the OpenMP runtime uses by default. */
+int gmlp_oracle_max_threads(void)
+{
+    return pick_threads(0);
+}
