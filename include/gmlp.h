@@ -1,0 +1,140 @@
+/*
+ * gmlp.h -- C ABI of the MI355X (gfx950) SiLU Gated MLP library, libgmlp.so.
+ *
+ * The operation (the paper's "SiLU Gated MLP" benchmark; graph in Fig.
+ * fig:mlp-example, Section 4.1):
+ *
+ *     G = X Wg,   U = X Wu,   H = silu(G) * U,   Y = H Wd
+ *
+ * with matmul(a, b)[i, j] = sum_k a[i, k] b[k, j] (Fig. fig:op-sema,
+ * Section 4.2.1) and silu(x) = x * sigmoid(x) (table tab:nki-ops,
+ * Section 5.1).  W1, W2, W3 of the figure are Wg, Wu, Wd here.
+ *
+ * Numerics: every tensor is IEEE bfloat16 (bf16 bit patterns in uint16
+ * storage).  Products are accumulated in fp32; G and U stay in fp32 registers;
+ * silu is evaluated in fp32; H is rounded once to bf16 (round-to-nearest-even)
+ * when it is written, and Y is rounded once to bf16 from its fp32 accumulator.
+ *
+ * Layout: all tensors are dense and row-major on the current HIP device:
+ *     X  [T, D]     Wg [D, F]     Wu [D, F]     Wd [F, D]
+ *     H  [T, F]     Y  [T, D]
+ * T is the number of tokens (rows of X), D the model width, F the hidden
+ * width.  D and F must be multiples of 8 and every pointer 16-byte aligned
+ * (rows are then 16-byte aligned, which the kernels' 16-byte loads need).
+ *
+ * Ownership: the caller owns every tensor and every workspace; the library
+ * never frees, keeps or reallocates caller memory, and holds no pointer after
+ * a call returns.  Entry points without a workspace argument allocate their
+ * scratch stream-ordered (hipMallocAsync/hipFreeAsync on the given stream).
+ *
+ * Streams: `stream` is a hipStream_t (NULL = the null stream).  Every compute
+ * entry point only enqueues work and returns; kernel faults surface at the
+ * caller's next synchronisation.  Calls on one stream are ordered; two calls
+ * that share a workspace must not run concurrently (they would race on it).
+ *
+ * Errors: every entry point returns GMLP_OK (0) or a positive GMLP_ERR_*
+ * code, never throws, and stores a human-readable detail for the calling
+ * thread that gmlp_last_error() returns.  T == 0 is valid and launches
+ * nothing.
+ */
+#ifndef GMLP_H
+#define GMLP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GMLP_VERSION 100 /* 1.0.0 */
+
+enum gmlp_status {
+    GMLP_OK = 0,
+    GMLP_ERR_INVALID_ARG = 1, /* null pointer, negative or overflowing size, aliasing output */
+    GMLP_ERR_UNSUPPORTED = 2, /* D or F not a multiple of 8, misaligned pointer, size too large */
+    GMLP_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
+    GMLP_ERR_NO_MEMORY = 4,   /* scratch allocation failed, or workspace too small */
+};
+
+/* Which kernels compute the call (gmlp_forward_ex). */
+enum gmlp_path {
+    GMLP_PATH_AUTO = 0, /* GEMV for T <= 8, MFMA GEMMs otherwise */
+    GMLP_PATH_GEMV = 1, /* split-K streaming GEMV kernels; needs T <= 8 */
+    GMLP_PATH_MFMA = 2, /* MFMA GEMM kernels (any T) */
+};
+
+/* Library version, GMLP_VERSION of the build. */
+int gmlp_version(void);
+
+/* Static name of a status code ("GMLP_OK", ...); never NULL. */
+const char *gmlp_status_string(int status);
+
+/* Detail of the last error returned to the calling thread ("" if none).
+ * The string is owned by the library and valid until the thread's next call. */
+const char *gmlp_last_error(void);
+
+/*
+ * Host-only check of the arguments of gmlp_forward: sizes (T >= 0, D > 0,
+ * F > 0, D % 8 == 0, F % 8 == 0, element counts that fit in int64 and in the
+ * kernels' 32-bit tile offsets), non-NULL 16-byte aligned pointers, and Y not
+ * overlapping any input.  Touches no device memory and makes no HIP call.
+ */
+int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg,
+                  const void *Wu, const void *Wd, const void *Y);
+
+/*
+ * Bytes of workspace gmlp_forward_ws / gmlp_forward_ex need for this shape
+ * (for any path).  The workspace holds H [T, F] bf16, fp32 split-K partial
+ * sums and a block of arrival counters.  0 if the shape is invalid.
+ */
+size_t gmlp_workspace_size(int64_t T, int64_t D, int64_t F);
+
+/*
+ * Prepare a workspace of `bytes` bytes for its first use: zero its counter
+ * block (stream-ordered on `stream`).  The kernels return every counter to
+ * zero when they finish, so this is needed once per fresh buffer, not per
+ * call.  A buffer that was zero-filled by other means needs no init.
+ */
+int gmlp_workspace_init(void *workspace, size_t bytes, void *stream);
+
+/*
+ * Y = (silu(X Wg) * (X Wu)) Wd  for X [T, D], Wg/Wu [D, F], Wd [F, D],
+ * Y [T, D], all bf16 device pointers (see the header comment for layout and
+ * numerics).  Allocates its scratch stream-ordered on `stream`.
+ */
+int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                 int64_t T, int64_t D, int64_t F, void *stream);
+
+/*
+ * gmlp_forward with a caller-provided workspace of `ws_bytes` >=
+ * gmlp_workspace_size(T, D, F) bytes, 256-byte aligned, prepared once with
+ * gmlp_workspace_init.  Allocates nothing.
+ */
+int gmlp_forward_ws(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                    int64_t T, int64_t D, int64_t F, void *workspace, size_t ws_bytes,
+                    void *stream);
+
+/* gmlp_forward_ws with the kernel path chosen explicitly (enum gmlp_path). */
+int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                    int64_t T, int64_t D, int64_t F, int path, void *workspace,
+                    size_t ws_bytes, void *stream);
+
+/*
+ * First half of the graph alone (the paper's "MM+MM+SiLU+Mul" kernel):
+ * H = bf16(silu(X Wg) * (X Wu)), H [T, F].  Allocates its scratch
+ * stream-ordered on `stream`.
+ */
+int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t T,
+                 int64_t D, int64_t F, void *stream);
+
+/* Down projection alone: Y = bf16(H Wd), H [T, F], Wd [F, D], Y [T, D].
+ * Allocates its scratch stream-ordered on `stream`. */
+int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D,
+              void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GMLP_H */

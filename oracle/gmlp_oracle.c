@@ -204,6 +204,43 @@ int gmlp_oracle_rows_f64(const double *X, const double *Wg, const double *Wu,
     ORACLE_DRIVER(f64, double)
 }
 
+/*
+ * Step 4 alone, on given rows of a bf16 H [T, F]: Y[r, :] = H[rows[r], :] Wd
+ * with Wd [F, D] (the down projection of the graph, checked by itself).
+ * Same return codes as above.
+ */
+int gmlp_oracle_down_rows_bf16(const uint16_t *H, const uint16_t *Wd, int64_t T, int64_t F,
+                               int64_t D, const int64_t *rows, int64_t n, double *Y,
+                               int threads)
+{
+    if (D <= 0 || F <= 0 || T < 0 || n < 0 || !H || !Wd || !Y)
+        return 1;
+    for (int64_t r = 0; r < n; ++r) {
+        int64_t t = rows ? rows[r] : r;
+        if (t < 0 || t >= T)
+            return 2;
+    }
+    int nthr = pick_threads(threads);
+    double *h = (double *)malloc(sizeof(double) * (size_t)n * (size_t)F);
+    if (!h)
+        return 3;
+    for (int64_t r = 0; r < n; ++r) {
+        int64_t t = rows ? rows[r] : r;
+        for (int64_t f = 0; f < F; ++f)
+            h[r * F + f] = ld_bf16(H, t * F + f);
+    }
+    int64_t dc = n >= nthr ? D : CHUNK;
+    int64_t ndc = (D + dc - 1) / dc;
+#pragma omp parallel for num_threads(nthr) schedule(dynamic, 1)
+    for (int64_t task = 0; task < n * ndc; ++task) {
+        int64_t r = task / ndc, j_lo = (task % ndc) * dc;
+        int64_t j_hi = j_lo + dc < D ? j_lo + dc : D;
+        down_bf16(h + r * F, Wd, F, D, j_lo, j_hi, Y + r * D);
+    }
+    free(h);
+    return 0;
+}
+
 /* Number of threads the OpenMP runtime uses by default. */
 int gmlp_oracle_max_threads(void)
 {

@@ -54,6 +54,9 @@ class Oracle:
             fn = getattr(lib, name)
             fn.argtypes = [_P, _P, _P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, ctypes.c_int]
             fn.restype = ctypes.c_int
+        lib.gmlp_oracle_down_rows_bf16.argtypes = [_P, _P, _I64, _I64, _I64, _P, _I64, _P,
+                                                   ctypes.c_int]
+        lib.gmlp_oracle_down_rows_bf16.restype = ctypes.c_int
         lib.gmlp_oracle_max_threads.argtypes = []
         lib.gmlp_oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
@@ -112,6 +115,27 @@ class Oracle:
         if rc != 0:
             raise RuntimeError("oracle returned error code %d" % rc)
         return (Y, H) if return_h else Y
+
+
+    def down_rows(self, H, Wd, rows: Optional[Sequence[int]] = None, threads: int = 0):
+        """Rows of H Wd in double precision for bf16 bit patterns H [T, F] and
+        Wd [F, D] (the down projection alone)."""
+        H = np.ascontiguousarray(H, dtype=np.uint16)
+        Wd = np.ascontiguousarray(Wd, dtype=np.uint16)
+        T, F = H.shape
+        if Wd.shape[0] != F:
+            raise ValueError("shape mismatch: H %s Wd %s" % (H.shape, Wd.shape))
+        D = Wd.shape[1]
+        rows_arr = (np.arange(T, dtype=np.int64) if rows is None
+                    else np.ascontiguousarray(np.asarray(rows, dtype=np.int64).reshape(-1)))
+        n = rows_arr.size
+        Y = np.zeros((n, D), dtype=np.float64)
+        rc = self.lib.gmlp_oracle_down_rows_bf16(H.ctypes.data, Wd.ctypes.data, T, F, D,
+                                                 rows_arr.ctypes.data if n else None, n,
+                                                 Y.ctypes.data, int(threads))
+        if rc != 0:
+            raise RuntimeError("oracle returned error code %d" % rc)
+        return Y
 
 
 _DEFAULT: Optional[Oracle] = None

@@ -1,0 +1,63 @@
+"""Build libgmlp.so (HIP, gfx950) in-tree with hipcc.
+
+    python -m paper_2606_26344_amd.build
+
+The library is compiled for gfx950 only.  Packed fp32 instructions are
+disabled for all device code (-packed-fp32-ops).
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIBRARY = os.path.join(PKG, "libgmlp.so")
+SOURCES = [os.path.join(CSRC, "gmlp.hip")]
+HEADERS = [os.path.join(CSRC, f) for f in ("common.hpp", "gemm_mfma.hpp", "gemv.hpp")] + [
+    os.path.join(INCLUDE, "gmlp.h")]
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+FLAGS = [
+    "--offload-arch=gfx950",
+    "-O3",
+    "-std=c++20",
+    "-shared",
+    "-fPIC",
+    "-Wall",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", INCLUDE,
+    "-I", CSRC,
+]
+
+
+def build(verbose: bool = False, extra_flags=()) -> str:
+    """Compile libgmlp.so next to this file; returns its path."""
+    tmp = LIBRARY + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, *FLAGS, *extra_flags, "-o", tmp, *SOURCES]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    noise = "warning: unknown target feature"
+    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if ln.strip()]
+    shown = [ln for ln in msgs if noise not in ln and "packed-fp32-ops" not in ln]
+    if shown and (verbose or res.returncode != 0):
+        print("\n".join(shown), file=sys.stderr)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed with exit code %d" % res.returncode)
+    os.replace(tmp, LIBRARY)
+    return LIBRARY
+
+
+def is_stale() -> bool:
+    if not os.path.exists(LIBRARY):
+        return True
+    t = os.path.getmtime(LIBRARY)
+    return any(os.path.getmtime(f) > t for f in SOURCES + HEADERS)
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

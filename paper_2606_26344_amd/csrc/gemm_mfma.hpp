@@ -1,0 +1,401 @@
+// MFMA GEMM kernels of the Gated MLP for gfx950 (CDNA4).
+//
+// One template computes   C[n, m] = sum_k act[n, k] * W[k, m]
+// for row-major activations act [N, K] (K contiguous) and weights W [K, M]
+// (M contiguous), i.e. the matmuls of the Gated MLP graph (Fig.
+// fig:mlp-example, Section 4.1) with N = tokens.  Two instantiations matter:
+//
+//   * dual-B gate/up:  NW = 2 weights (Wg, Wu) share every staged tile of X
+//     (the paper's fusion of independent matmuls into one loop nest,
+//     Section 4.5), and the epilogue writes H = bf16(silu(G) * U) straight
+//     from the fp32 accumulators; G and U never leave registers.
+//   * down:            NW = 1 (Wd), epilogue writes Y = bf16(H Wd).
+//
+// Data flow per k-step of 64:
+//   global --(buffer_load ... lds, 16 B per lane, zero-filled out of range)-->
+//   LDS (STAGES-deep ring; 16-byte chunks XOR-swizzled so that the fragment
+//   reads below are free of bank conflicts) --> registers --> MFMA.
+//
+// Operand roles.  v_mfma_f32_32x32x16_bf16 needs both operands K-contiguous
+// per lane.  The activations are stored K-contiguous and are read with
+// ds_read_b128.  The weights are stored M-contiguous, so they are read with
+// the gfx950 transposing LDS load ds_read_b64_tr_b16: each 16-lane group
+// fetches a 4 (k) x 16 (m) block and each lane receives one column's 4 k
+// values.  The transpose thus happens inside the LDS read, never as a pass
+// over memory (the paper fuses the transpose its matmul instruction needs
+// into the data movement, Sections 4.4-4.5).
+//
+// The weights are the MFMA "A" operand (rows m) and the tokens the "B"
+// operand (columns n), so the accumulator of a lane holds, for one token,
+// runs of 4 consecutive output columns: the result is produced already in
+// the row-major [N, M] layout of H and Y and is stored as 8-byte rows
+// without any transpose (the operand swap the paper derives for
+// transpose(nc_matmul(a, b)), Section 4.5).
+#pragma once
+
+#include <utility>
+
+#include "common.hpp"
+
+namespace gmlp {
+
+struct GemmParams {
+    const uint16_t *w0;  // [K, M] bf16, M contiguous (Wg, or Wd)
+    const uint16_t *w1;  // [K, M] bf16 second weight (Wu) of the dual kernel
+    const uint16_t *act; // [N, K] bf16, K contiguous (X, or H)
+    uint16_t *out;       // [N, M] bf16 (H, or Y)
+    float *partial;      // split-K partial sums [splits][NW][N][M] fp32
+    uint32_t *counters;  // split-K arrival counter per output tile (zero on entry and exit)
+    int M, N, K;
+    int k_split; // K rows per split (a multiple of 64 when splits > 1)
+    int splits;
+    int tiles_m, tiles_n;
+};
+
+template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_>
+struct GemmShape {
+    static constexpr int NW = NW_, WM = WM_, WN = WN_, TM = TM_, TN = TN_, STAGES = STAGES_;
+    static constexpr int BK = 64;
+    static constexpr int NWAVES = WM * WN;
+    static constexpr int NTHREADS = NWAVES * 64;
+    static constexpr int BMW = WM * TM * 32;       // columns per weight per tile
+    static constexpr int BN = WN * TN * 32;        // tokens per tile
+    static constexpr int W_ROW_BYTES = BMW * 2;    // one k row of a weight tile
+    static constexpr int W_CPR = BMW / 8;          // 16-byte chunks per weight row
+    static constexpr int W_TILE_BYTES = BK * BMW * 2;
+    static constexpr int X_TILE_BYTES = BN * BK * 2;
+    static constexpr int STAGE_BYTES = NW * W_TILE_BYTES + X_TILE_BYTES;
+    static constexpr int W_LOADS = W_TILE_BYTES / (NTHREADS * 16); // per weight, per thread
+    static constexpr int X_LOADS = X_TILE_BYTES / (NTHREADS * 16);
+    static constexpr int LOADS_PER_STAGE = NW * W_LOADS + X_LOADS;
+    static constexpr int W_LPR = 64 / W_CPR;          // weight rows per wave load
+    static constexpr int W_RPI = NWAVES * W_LPR;      // weight rows per load step i
+    static_assert(BMW >= 64, "weight rows of at least 8 chunks");
+    static_assert(W_TILE_BYTES % (NTHREADS * 16) == 0 && X_TILE_BYTES % (NTHREADS * 16) == 0,
+                  "every thread issues whole 16-byte loads");
+    static_assert(STAGES >= 2 && STAGES <= 4, "2..4 LDS stages");
+    static_assert((STAGES - 2) * LOADS_PER_STAGE < 64, "vmcnt range");
+    static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS capacity of a CU");
+};
+
+// Physical 16-byte chunk of logical chunk c in row k of a weight tile.  The
+// XOR keeps the 4 rows x 4 chunks read by 32 lanes of one transposing load
+// on distinct banks (and the 4 x 2 read by 16 lanes), for 64 or 32 banks.
+template <int CPR>
+__device__ __forceinline__ int w_swizzle(int k)
+{
+    if constexpr (CPR >= 16) {
+        const int g = k & 3;
+        return g == 0 ? 0 : g == 1 ? 6 : g == 2 ? 10 : 12;
+    } else {
+        return (k & 3) << 1;
+    }
+}
+
+// Physical chunk of logical chunk c (0..7) in token row t of an activation
+// tile: any 8 (and any aligned 16) consecutive rows reading one logical chunk
+// hit distinct banks.
+__device__ __forceinline__ int x_swizzle(int t) { return (t ^ (t >> 3)) & 7; }
+
+// SPLIT selects the split-K variant (several blocks per output tile, summed
+// by the last one); without it p.splits must be 1.
+template <class S, int EPI, bool SPLIT>
+__global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
+{
+    constexpr int NW = S::NW, TM = S::TM, TN = S::TN, STAGES = S::STAGES;
+    constexpr int NWAVES = S::NWAVES;
+    // One LDS array per pipeline stage: distinct objects let the compiler see
+    // that reading one stage does not depend on the DMA into another.
+    __shared__ __attribute__((aligned(1024))) uint8_t lds0[S::STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds1[S::STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds2[STAGES > 2 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds3[STAGES > 3 ? S::STAGE_BYTES : 16];
+    __shared__ int s_last;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % S::WM, wn = wave / S::WM;
+
+    const int ntiles = p.tiles_m * p.tiles_n;
+    const int id = xcd_contiguous_id(blockIdx.x, ntiles * p.splits);
+    const int split = id / ntiles;
+    const int tile = id - split * ntiles;
+    const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
+    const int M = p.M, N = p.N, K = p.K;
+    const int m0 = tm * S::BMW, n0 = tn * S::BN;
+    const int kb = split * p.k_split;
+    const int ke = min(K, kb + p.k_split);
+    const int nk = (ke - kb + S::BK - 1) / S::BK;
+    const bool ragged_k = (ke - kb) % S::BK != 0; // last k-tile is partial
+
+    auto stage_ptr = [&](auto s) __attribute__((always_inline)) -> uint8_t * {
+        if constexpr (decltype(s)::value == 0) return lds0;
+        else if constexpr (decltype(s)::value == 1) return lds1;
+        else if constexpr (decltype(s)::value == 2) return lds2;
+        else return lds3;
+    };
+
+    // ---- staging addresses ---------------------------------------------------
+    // Weight load i of this lane: row i*W_RPI + w_k, physical chunk lane %
+    // W_CPR holding logical chunk w_c.  The swizzle depends on the row only
+    // through row % 4, which is the same for every i, so one voffset serves
+    // all i and the row step goes into the scalar offset.
+    const int w_k = wave * S::W_LPR + lane / S::W_CPR;
+    const int w_c = (lane % S::W_CPR) ^ w_swizzle<S::W_CPR>(w_k);
+    const bool w_col_ok = m0 + w_c * 8 < M;
+    const uint32_t w_voff = w_col_ok ? (uint32_t)(w_k * M + w_c * 8) * 2u : kOutOfRange;
+    const uint32_t w_soff_step = (uint32_t)S::W_RPI * (uint32_t)M * 2u;
+    // Activation load i: token row x_t(i), chunk x_c(i).  Rows past N are
+    // clamped to N-1: they only feed output rows that are never stored.
+    uint32_t x_voff[S::X_LOADS];
+#pragma unroll
+    for (int i = 0; i < S::X_LOADS; ++i) {
+        const int t = (i * NWAVES + wave) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ x_swizzle(t);
+        x_voff[i] = (uint32_t)((min(n0 + t, N - 1) - n0) * K + c * 8) * 2u;
+    }
+
+    // Issue the DMA of k-tile kt into stage buffer sbuf.  Only a partial last
+    // tile needs per-lane k masks (rows of W and columns of act past the end
+    // of the k range read as zeros).
+    auto issue = [&](uint8_t *sbuf, int kt) __attribute__((always_inline)) {
+        const int k0 = kb + kt * S::BK;
+        const int krem = ke - k0;
+        const bool tail = ragged_k && kt == nk - 1;
+        const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.act + (size_t)n0 * K + k0);
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? p.w0 : p.w1) + (size_t)k0 * M + m0);
+#pragma unroll
+            for (int i = 0; i < S::W_LOADS; ++i) {
+                const uint32_t v = (tail && i * S::W_RPI + w_k >= krem) ? kOutOfRange : w_voff;
+                load16_to_lds(rw, sbuf + w * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v,
+                              (uint32_t)i * w_soff_step);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < S::X_LOADS; ++i) {
+            uint32_t v = x_voff[i];
+            if (tail) {
+                const int t = (i * NWAVES + wave) * 8 + (lane >> 3);
+                const int c = (lane & 7) ^ x_swizzle(t);
+                v = c * 8 < krem ? v : kOutOfRange;
+            }
+            load16_to_lds(rx, sbuf + NW * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v);
+        }
+    };
+
+    // ---- fragment read offsets ---------------------------------------------
+    // Weight (A) fragment of m-tile mi for k16 step kk: a transposing read of
+    // k rows kk*16 + r_lane (+4 for elements 4..7) in column chunk c.
+    const int r_lane = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    int a_off[TM];
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi) {
+        const int c = wm * TM * 4 + mi * 4 + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+        a_off[mi] = r_lane * S::W_ROW_BYTES + ((c ^ w_swizzle<S::W_CPR>(r_lane)) << 4) + (lane & 1) * 8;
+    }
+    // Token (B) fragment of n-tile ni: row t = wn*TN*32 + ni*32 + lane%32,
+    // logical chunk 2*kk + lane/32.  The row bits of the swizzle differ
+    // between even and odd ni only, and rows are 128 bytes, so the byte
+    // address is (b_base[ni & 1] + ni*4096) ^ (32*kk).
+    int b_base[2];
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+        const int t = wn * TN * 32 + par * 32 + (lane & 31);
+        b_base[par] = t * 128 + ((((lane >> 5) ^ x_swizzle(t))) << 4) - par * 4096;
+    }
+
+    f32x16 acc[NW][TM][TN];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < TN; ++ni)
+                acc[w][mi][ni] = f32x16{};
+
+    struct Frags {
+        bf16x8 a[NW][TM];
+        bf16x8 b[TN];
+    };
+    auto load_frags = [&](Frags &f, const uint8_t *sbuf, int kk) __attribute__((always_inline)) {
+        const uint8_t *sx = sbuf + NW * S::W_TILE_BYTES;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi) {
+                const uint8_t *pa = sbuf + w * S::W_TILE_BYTES + kk * 16 * S::W_ROW_BYTES + a_off[mi];
+                i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa));
+                i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa + 4 * S::W_ROW_BYTES));
+                f.a[w][mi] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            }
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni) {
+            const int off = (b_base[ni & 1] + ni * 4096) ^ (32 * kk);
+            f.b[ni] = *(const bf16x8 *)(sx + off);
+        }
+    };
+    auto mma = [&](const Frags &f) __attribute__((always_inline)) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < TN; ++ni)
+                    acc[w][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[w][mi], f.b[ni],
+                                                                             acc[w][mi][ni], 0, 0, 0);
+    };
+    // Tile kt has landed in LDS (for every wave) once at most the tiles
+    // issued after it are in flight and all waves have passed a barrier.
+    auto wait_tile = [&](int kt) __attribute__((always_inline)) {
+        if (kt + STAGES - 2 < nk)
+            wait_vmcnt<(STAGES - 2) * S::LOADS_PER_STAGE>();
+        else
+            wait_vmcnt<0>();
+        wait_lgkm0();
+        barrier_only();
+    };
+
+    // ---- pipelined main loop -------------------------------------------------
+    // Stage buffer of tile kt is kt % STAGES.  Fragments are double-buffered
+    // in registers: the reads for k16 step kk+1 are issued before the MFMAs
+    // of step kk.  At the last step of a tile the next tile's first
+    // fragments are read after the barrier that also frees this tile's
+    // buffer for the DMA of tile kt + STAGES.
+    Frags f0, f1;
+    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+        ((I < nk ? issue(stage_ptr(std::integral_constant<int, I>{}), I) : void()), ...);
+    }(std::make_integer_sequence<int, STAGES - 1>{});
+    if (nk > 0) {
+        wait_tile(0);
+        if (STAGES - 1 < nk)
+            issue(stage_ptr(std::integral_constant<int, STAGES - 1>{}), STAGES - 1);
+    }
+    load_frags(f0, lds0, 0);
+
+    // One k-tile held in stage buffer I.  Only uniform branches around
+    // side-effecting work (waits, DMA issue): the registers flow straight
+    // through, so accumulators and fragments need no copies.  At the last
+    // tile the next-tile fragment read touches stale LDS and is unused.
+    auto step = [&](auto stage, int kt) __attribute__((always_inline)) {
+        constexpr int I = decltype(stage)::value;
+        uint8_t *buf = stage_ptr(stage);
+        load_frags(f1, buf, 1);
+        mma(f0);
+        load_frags(f0, buf, 2);
+        mma(f1);
+        load_frags(f1, buf, 3);
+        mma(f0);
+        if (kt + 1 < nk) {
+            wait_tile(kt + 1);
+            if (kt + STAGES < nk)
+                issue(buf, kt + STAGES);
+        }
+        load_frags(f0, stage_ptr(std::integral_constant<int, (I + 1) % STAGES>{}), 0);
+        mma(f1);
+    };
+    int kt = 0;
+    for (; kt + STAGES <= nk; kt += STAGES) {
+        [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+            (step(std::integral_constant<int, I>{}, kt + I), ...);
+        }(std::make_integer_sequence<int, STAGES>{});
+    }
+    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+        ((kt + I < nk ? step(std::integral_constant<int, I>{}, kt + I) : void()), ...);
+    }(std::make_integer_sequence<int, STAGES - 1>{});
+
+    // ---- split-K: fixed-order reduction by the last block of each tile ----------
+    if (SPLIT && p.splits > 1) {
+        const size_t plane = (size_t)N * M;
+        float *mine = p.partial + (size_t)split * NW * plane;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+                        if (t < N && f < M) {
+                            f32x4 v = {acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
+                                       acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
+                            *(f32x4 *)(mine + w * plane + (size_t)t * M + f) = v;
+                        }
+                    }
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) {
+            const uint32_t before =
+                __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = before == (uint32_t)(p.splits - 1);
+        }
+        __syncthreads();
+        if (!s_last)
+            return;
+        __threadfence();
+        if (tid == 0)
+            __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+                        if (t < N && f < M) {
+                            f32x4 sum = {};
+                            for (int s = 0; s < p.splits; ++s) {
+                                f32x4 v;
+                                if (s == split)
+                                    v = f32x4{acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
+                                              acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
+                                else
+                                    v = __builtin_nontemporal_load(
+                                        (const f32x4 *)(p.partial + ((size_t)s * NW + w) * plane +
+                                                        (size_t)t * M + f));
+                                sum = s == 0 ? v : sum + v;
+                            }
+                            acc[w][mi][ni][4 * j] = sum[0];
+                            acc[w][mi][ni][4 * j + 1] = sum[1];
+                            acc[w][mi][ni][4 * j + 2] = sum[2];
+                            acc[w][mi][ni][4 * j + 3] = sum[3];
+                        }
+                    }
+    }
+
+    // ---- epilogue: fp32 -> (silu(G) * U) -> bf16, 8-byte row-major stores -----
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+                if (t < N && f < M) {
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if constexpr (EPI == EPI_SILU_MUL)
+                            v[e] = silu(acc[0][mi][ni][4 * j + e]) * acc[NW - 1][mi][ni][4 * j + e];
+                        else
+                            v[e] = acc[0][mi][ni][4 * j + e];
+                    }
+                    u32x2 packed = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                    *(u32x2 *)(p.out + (size_t)t * M + f) = packed;
+                }
+                // Keep the scheduler from pulling every accumulator out of
+                // the AGPRs at once.
+                __builtin_amdgcn_sched_barrier(0);
+            }
+}
+
+} // namespace gmlp

@@ -1,0 +1,502 @@
+// libgmlp.so: the C ABI of include/gmlp.h on top of the gfx950 kernels.
+//
+// Host side only: argument validation, the choice of kernels and tile
+// configuration for a shape (the library's static analogue of the paper's
+// empirical per-shape selection, Section 4.6), workspace layout and launches.
+// Every arithmetic step of the Gated MLP runs in the kernels of
+// gemm_mfma.hpp and gemv.hpp.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "gmlp.h"
+#include "gemm_mfma.hpp"
+#include "gemv.hpp"
+
+using namespace gmlp;
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok()
+{
+    g_err[0] = '\0';
+    return GMLP_OK;
+}
+
+// ---- tile configurations -------------------------------------------------
+//                       NW WM WN TM TN STAGES
+using GateUpLarge = GemmShape<2, 2, 2, 2, 4, 2>; // 128 F cols x 256 tokens, per weight
+using GateUpSmall = GemmShape<2, 2, 2, 1, 2, 4>; //  64 F cols x 128 tokens
+using DownLarge = GemmShape<1, 2, 2, 4, 4, 2>;   // 256 D cols x 256 tokens
+using DownSmall = GemmShape<1, 2, 2, 2, 2, 4>;   // 128 D cols x 128 tokens
+
+constexpr int kGemvMaxTokens = 8;
+constexpr int64_t kMaxDim = int64_t(1) << 22; // D, F: keeps 32-bit tile offsets in range
+constexpr int64_t kMaxTokens = int64_t(1) << 30;
+constexpr size_t kAlign = 256;
+// Arrival counters sit at the start of every workspace in a block of fixed
+// size (enough for any shape: at most kMaxDim / 256 GEMV strips, fewer than
+// 256 split GEMM tiles), so a zeroed workspace stays valid when it is reused
+// for another shape.
+constexpr size_t kCounterBytes = 64 * 1024;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+enum Kind { K_NONE, K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_DN_L, K_GEMM_DN_S, K_GEMV };
+
+// One matmul step (gate/up or down) of a call.
+struct Step {
+    Kind kind = K_NONE;
+    int M = 0, N = 0, K = 0;
+    int tiles_m = 0, tiles_n = 0; // GEMM
+    int strips = 0;               // GEMV
+    int splits = 1, k_split = 0;
+    int blocks = 0, threads = 0;
+    size_t partial_bytes = 0; // fp32 split-K partial sums
+    int counters = 0;         // arrival counters
+};
+
+struct Plan {
+    int path = GMLP_PATH_AUTO;
+    Step gate_up, down;
+};
+
+struct Layout {
+    size_t counters_off = 0, h_off = 0, partial_off = 0, total = 0;
+    int counters = 0; // most arrival counters any path uses for this shape
+};
+
+// Split K so that about `target` blocks run, keeping at least `min_tiles`
+// k-tiles of `tile_k` rows per split.
+void choose_splits(Step &s, int tiles, int target, int tile_k, int min_tiles)
+{
+    const int64_t ktiles = cdiv(s.K, tile_k);
+    int64_t splits = 1;
+    if (tiles < target)
+        splits = std::min<int64_t>(cdiv(target, tiles), std::max<int64_t>(1, ktiles / min_tiles));
+    const int64_t per = cdiv(ktiles, splits);
+    s.k_split = (int)(per * tile_k);
+    s.splits = (int)cdiv(s.K, s.k_split);
+}
+
+template <class S>
+void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split)
+{
+    s.kind = kind;
+    s.M = M;
+    s.N = N;
+    s.K = K;
+    s.tiles_m = (int)cdiv(M, S::BMW);
+    s.tiles_n = (int)cdiv(N, S::BN);
+    const int tiles = s.tiles_m * s.tiles_n;
+    if (allow_split)
+        choose_splits(s, tiles, 256, S::BK, 2);
+    else {
+        s.splits = 1;
+        s.k_split = K;
+    }
+    s.blocks = tiles * s.splits;
+    s.threads = S::NTHREADS;
+    s.counters = s.splits > 1 ? tiles : 0;
+    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
+}
+
+void gemv_step(Step &s, int M, int N, int K, int nw)
+{
+    s.kind = K_GEMV;
+    s.M = M;
+    s.N = N;
+    s.K = K;
+    s.strips = (int)cdiv(M, kGemvStrip);
+    // About four blocks per CU, split rows a multiple of 8, at most the LDS copy.
+    int64_t splits = std::max<int64_t>(1, cdiv(1024, s.strips));
+    int64_t per = std::max<int64_t>(8, cdiv(cdiv(K, splits), 8) * 8);
+    per = std::min<int64_t>(per, kGemvMaxSplitRows);
+    s.k_split = (int)per;
+    s.splits = (int)cdiv(K, per);
+    s.blocks = s.strips * s.splits;
+    s.threads = kGemvThreads;
+    s.counters = s.splits > 1 ? s.strips : 0;
+    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
+}
+
+Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
+{
+    Plan p;
+    if (path == GMLP_PATH_AUTO)
+        path = T <= kGemvMaxTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
+    p.path = path;
+    if (path == GMLP_PATH_GEMV) {
+        gemv_step(p.gate_up, (int)F, (int)T, (int)D, 2);
+        gemv_step(p.down, (int)D, (int)T, (int)F, 1);
+        return p;
+    }
+    // Gate/up: large tiles once there are enough of them to fill the chip.
+    if (cdiv(T, GateUpLarge::BN) * cdiv(F, GateUpLarge::BMW) >= 512)
+        gemm_step<GateUpLarge>(p.gate_up, K_GEMM_GU_L, (int)F, (int)T, (int)D, 2, false);
+    else
+        gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true);
+    if (cdiv(T, DownLarge::BN) * cdiv(D, DownLarge::BMW) >= 192)
+        gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false);
+    else
+        gemm_step<DownSmall>(p.down, K_GEMM_DN_S, (int)D, (int)T, (int)F, 1, true);
+    return p;
+}
+
+// One layout serves every path, so a workspace sized by gmlp_workspace_size
+// fits whichever kernels run.
+Layout make_layout(int64_t T, int64_t D, int64_t F)
+{
+    int counters = 0;
+    size_t partial = 0;
+    for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {
+        if (path == GMLP_PATH_GEMV && T > kGemvMaxTokens)
+            continue;
+        const Plan p = make_plan(T, D, F, path);
+        counters = std::max({counters, p.gate_up.counters, p.down.counters});
+        partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes});
+    }
+    Layout l;
+    l.counters_off = 0;
+    l.h_off = kCounterBytes;
+    l.counters = counters;
+    l.partial_off = l.h_off + align_up((size_t)T * F * 2);
+    l.total = l.partial_off + align_up(partial);
+    return l;
+}
+
+bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
+
+bool overlaps(const void *a, size_t an, const void *b, size_t bn)
+{
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return an && bn && x < y + bn && y < x + an;
+}
+
+int check_shape(int64_t T, int64_t D, int64_t F)
+{
+    if (T < 0 || D <= 0 || F <= 0)
+        return fail(GMLP_ERR_INVALID_ARG, "invalid shape T=%lld D=%lld F=%lld (need T >= 0, D > 0, F > 0)",
+                    (long long)T, (long long)D, (long long)F);
+    if (D % 8 || F % 8)
+        return fail(GMLP_ERR_UNSUPPORTED, "D=%lld and F=%lld must be multiples of 8", (long long)D,
+                    (long long)F);
+    if (D > kMaxDim || F > kMaxDim || T > kMaxTokens)
+        return fail(GMLP_ERR_UNSUPPORTED, "shape T=%lld D=%lld F=%lld exceeds the supported range "
+                    "(D, F <= %lld, T <= %lld)", (long long)T, (long long)D, (long long)F,
+                    (long long)kMaxDim, (long long)kMaxTokens);
+    return GMLP_OK;
+}
+
+int check_ptr(const void *p, const char *name, bool required)
+{
+    if (!p)
+        return required ? fail(GMLP_ERR_INVALID_ARG, "%s is NULL", name) : GMLP_OK;
+    if (misaligned(p))
+        return fail(GMLP_ERR_UNSUPPORTED, "%s (%p) is not 16-byte aligned", name, p);
+    return GMLP_OK;
+}
+
+int validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg, const void *Wu,
+             const void *Wd, const void *Y)
+{
+    int rc;
+    if ((rc = check_shape(T, D, F)))
+        return rc;
+    const bool rows = T > 0;
+    if ((rc = check_ptr(X, "X", rows)) || (rc = check_ptr(Wg, "Wg", true)) ||
+        (rc = check_ptr(Wu, "Wu", true)) || (rc = check_ptr(Wd, "Wd", true)) ||
+        (rc = check_ptr(Y, "Y", rows)))
+        return rc;
+    const size_t xb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
+    if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, Wg, wb) || overlaps(Y, xb, Wu, wb) ||
+        overlaps(Y, xb, Wd, wb))
+        return fail(GMLP_ERR_INVALID_ARG, "Y overlaps an input");
+    return GMLP_OK;
+}
+
+int hip_check(hipError_t e, const char *what)
+{
+    if (e != hipSuccess)
+        return fail(GMLP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return GMLP_OK;
+}
+
+// ---- launches ----------------------------------------------------------------
+
+template <class S, int EPI, bool SPLIT>
+int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                uint8_t *ws, const Layout &l, hipStream_t stream)
+{
+    GemmParams p;
+    p.w0 = static_cast<const uint16_t *>(w0);
+    p.w1 = static_cast<const uint16_t *>(w1);
+    p.act = static_cast<const uint16_t *>(act);
+    p.out = static_cast<uint16_t *>(out);
+    p.partial = reinterpret_cast<float *>(ws + l.partial_off);
+    p.counters = reinterpret_cast<uint32_t *>(ws + l.counters_off);
+    p.M = s.M;
+    p.N = s.N;
+    p.K = s.K;
+    p.k_split = s.k_split;
+    p.splits = s.splits;
+    p.tiles_m = s.tiles_m;
+    p.tiles_n = s.tiles_n;
+    if (!SPLIT && s.splits != 1)
+        return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
+    hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
+    return hip_check(hipGetLastError(), "MFMA GEMM launch");
+}
+
+template <int NT, int NW, int EPI>
+int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                   uint8_t *ws, const Layout &l, hipStream_t stream)
+{
+    GemvParams p;
+    p.w0 = static_cast<const uint16_t *>(w0);
+    p.w1 = static_cast<const uint16_t *>(w1);
+    p.act = static_cast<const uint16_t *>(act);
+    p.out = static_cast<uint16_t *>(out);
+    p.partial = reinterpret_cast<float *>(ws + l.partial_off);
+    p.counters = reinterpret_cast<uint32_t *>(ws + l.counters_off);
+    p.M = s.M;
+    p.K = s.K;
+    p.k_split = s.k_split;
+    p.splits = s.splits;
+    p.strips = s.strips;
+    hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI>), dim3(s.blocks), dim3(kGemvThreads), 0,
+                       stream, p);
+    return hip_check(hipGetLastError(), "GEMV launch");
+}
+
+template <int NW, int EPI>
+int launch_gemv(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                uint8_t *ws, const Layout &l, hipStream_t stream)
+{
+    switch (s.N) {
+    case 1: return launch_gemv_nt<1, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 2: return launch_gemv_nt<2, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 3: return launch_gemv_nt<3, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 4: return launch_gemv_nt<4, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 5: return launch_gemv_nt<5, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 6: return launch_gemv_nt<6, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 7: return launch_gemv_nt<7, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 8: return launch_gemv_nt<8, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    default: return fail(GMLP_ERR_INVALID_ARG, "GEMV path needs 1 <= T <= 8 (T=%d)", s.N);
+    }
+}
+
+int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, void *H, uint8_t *ws,
+                const Layout &l, hipStream_t st)
+{
+    switch (s.kind) {
+    case K_GEMM_GU_L: return launch_gemm<GateUpLarge, EPI_SILU_MUL, false>(s, Wg, Wu, X, H, ws, l, st);
+    case K_GEMM_GU_S: return launch_gemm<GateUpSmall, EPI_SILU_MUL, true>(s, Wg, Wu, X, H, ws, l, st);
+    case K_GEMV: return launch_gemv<2, EPI_SILU_MUL>(s, Wg, Wu, X, H, ws, l, st);
+    default: return fail(GMLP_ERR_INVALID_ARG, "no gate/up kernel for this plan");
+    }
+}
+
+int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws, const Layout &l,
+             hipStream_t st)
+{
+    switch (s.kind) {
+    case K_GEMM_DN_L: return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, st);
+    case K_GEMM_DN_S: return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, st);
+    case K_GEMV: return launch_gemv<1, EPI_STORE>(s, Wd, nullptr, H, Y, ws, l, st);
+    default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
+    }
+}
+
+int check_path(int path, int64_t T)
+{
+    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA)
+        return fail(GMLP_ERR_INVALID_ARG, "unknown path %d", path);
+    if (path == GMLP_PATH_GEMV && T > kGemvMaxTokens)
+        return fail(GMLP_ERR_UNSUPPORTED, "GEMV path needs T <= %d (T=%lld)", kGemvMaxTokens,
+                    (long long)T);
+    return GMLP_OK;
+}
+
+int check_workspace(void *ws, size_t ws_bytes, const Layout &l)
+{
+    if (!ws)
+        return fail(GMLP_ERR_INVALID_ARG, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign)
+        return fail(GMLP_ERR_UNSUPPORTED, "workspace %p is not %zu-byte aligned", ws, kAlign);
+    if (ws_bytes < l.total)
+        return fail(GMLP_ERR_NO_MEMORY, "workspace of %zu bytes, %zu needed", ws_bytes, l.total);
+    if ((size_t)l.counters * sizeof(uint32_t) > kCounterBytes)
+        return fail(GMLP_ERR_UNSUPPORTED, "shape needs %d arrival counters, more than the %zu reserved",
+                    l.counters, kCounterBytes / sizeof(uint32_t));
+    return GMLP_OK;
+}
+
+// Stream-ordered scratch for the entry points that allocate.
+struct Scratch {
+    void *ptr = nullptr;
+    hipStream_t stream = nullptr;
+    ~Scratch()
+    {
+        if (ptr)
+            (void)hipFreeAsync(ptr, stream);
+    }
+    int alloc(size_t bytes, const Layout &l, hipStream_t st)
+    {
+        stream = st;
+        int rc = hip_check(hipMallocAsync(&ptr, bytes, st), "hipMallocAsync(workspace)");
+        if (rc) {
+            ptr = nullptr;
+            return rc == GMLP_ERR_HIP ? fail(GMLP_ERR_NO_MEMORY, "%s", g_err) : rc;
+        }
+        return hip_check(hipMemsetAsync(ptr, 0, l.h_off, st), "hipMemsetAsync(counters)");
+    }
+};
+
+} // namespace
+
+extern "C" {
+
+int gmlp_version(void) { return GMLP_VERSION; }
+
+const char *gmlp_status_string(int status)
+{
+    switch (status) {
+    case GMLP_OK: return "GMLP_OK";
+    case GMLP_ERR_INVALID_ARG: return "GMLP_ERR_INVALID_ARG";
+    case GMLP_ERR_UNSUPPORTED: return "GMLP_ERR_UNSUPPORTED";
+    case GMLP_ERR_HIP: return "GMLP_ERR_HIP";
+    case GMLP_ERR_NO_MEMORY: return "GMLP_ERR_NO_MEMORY";
+    default: return "GMLP_ERR_UNKNOWN";
+    }
+}
+
+const char *gmlp_last_error(void) { return g_err; }
+
+int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg, const void *Wu,
+                  const void *Wd, const void *Y)
+{
+    int rc = validate(T, D, F, X, Wg, Wu, Wd, Y);
+    return rc ? rc : ok();
+}
+
+size_t gmlp_workspace_size(int64_t T, int64_t D, int64_t F)
+{
+    if (check_shape(T, D, F))
+        return 0;
+    return make_layout(T, D, F).total;
+}
+
+int gmlp_workspace_init(void *workspace, size_t bytes, void *stream)
+{
+    if (!workspace)
+        return fail(GMLP_ERR_INVALID_ARG, "workspace is NULL");
+    // Only the counter block at the start must be zero.
+    const size_t n = std::min(bytes, kCounterBytes);
+    int rc = hip_check(hipMemsetAsync(workspace, 0, n, static_cast<hipStream_t>(stream)),
+                       "hipMemsetAsync(workspace)");
+    return rc ? rc : ok();
+}
+
+int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
+                    int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+{
+    int rc;
+    if ((rc = validate(T, D, F, X, Wg, Wu, Wd, Y)) || (rc = check_path(path, T)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    if ((rc = check_workspace(workspace, ws_bytes, l)))
+        return rc;
+    const Plan plan = make_plan(T, D, F, path);
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    void *H = ws + l.h_off;
+    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, ws, l, st)) ||
+        (rc = run_down(plan.down, H, Wd, Y, ws, l, st)))
+        return rc;
+    return ok();
+}
+
+int gmlp_forward_ws(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
+                    int64_t D, int64_t F, void *workspace, size_t ws_bytes, void *stream)
+{
+    return gmlp_forward_ex(X, Wg, Wu, Wd, Y, T, D, F, GMLP_PATH_AUTO, workspace, ws_bytes, stream);
+}
+
+int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
+                 int64_t D, int64_t F, void *stream)
+{
+    int rc;
+    if ((rc = validate(T, D, F, X, Wg, Wu, Wd, Y)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, static_cast<hipStream_t>(stream))))
+        return rc;
+    return gmlp_forward_ex(X, Wg, Wu, Wd, Y, T, D, F, GMLP_PATH_AUTO, s.ptr, l.total, stream);
+}
+
+int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
+                 int64_t F, void *stream)
+{
+    int rc;
+    if ((rc = check_shape(T, D, F)) || (rc = check_ptr(X, "X", T > 0)) ||
+        (rc = check_ptr(Wg, "Wg", true)) || (rc = check_ptr(Wu, "Wu", true)) ||
+        (rc = check_ptr(H, "H", T > 0)))
+        return rc;
+    const size_t hb = (size_t)T * F * 2, xb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
+    if (overlaps(H, hb, X, xb) || overlaps(H, hb, Wg, wb) || overlaps(H, hb, Wu, wb))
+        return fail(GMLP_ERR_INVALID_ARG, "H overlaps an input");
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    const Plan plan = make_plan(T, D, F, GMLP_PATH_AUTO);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, st)) ||
+        (rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(s.ptr), l, st)))
+        return rc;
+    return ok();
+}
+
+int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D, void *stream)
+{
+    int rc;
+    if ((rc = check_shape(T, D, F)) || (rc = check_ptr(H, "H", T > 0)) ||
+        (rc = check_ptr(Wd, "Wd", true)) || (rc = check_ptr(Y, "Y", T > 0)))
+        return rc;
+    const size_t hb = (size_t)T * F * 2, yb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
+    if (overlaps(Y, yb, H, hb) || overlaps(Y, yb, Wd, wb))
+        return fail(GMLP_ERR_INVALID_ARG, "Y overlaps an input");
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    const Plan plan = make_plan(T, D, F, GMLP_PATH_AUTO);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, st)) ||
+        (rc = run_down(plan.down, H, Wd, Y, static_cast<uint8_t *>(s.ptr), l, st)))
+        return rc;
+    return ok();
+}
+
+} // extern "C"

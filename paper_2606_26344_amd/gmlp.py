@@ -1,0 +1,214 @@
+"""Python binding of libgmlp.so (the C ABI declared in include/gmlp.h).
+
+Argument marshalling only: every step of the Gated MLP runs in the library's
+HIP kernels.  PyTorch supplies device memory and the current HIP stream.  The
+names mirror the C entry points:
+
+    forward(x, wg, wu, wd)   -> gmlp_forward / gmlp_forward_ex
+    gate_up(x, wg, wu)       -> gmlp_gate_up
+    down(h, wd)              -> gmlp_down
+
+Tensors are ``torch.bfloat16``, contiguous, on one HIP device, with shapes
+x [T, D], wg [D, F], wu [D, F], wd [F, D].  Loading fails loudly if the
+library has not been built (``python -m paper_2606_26344_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(HERE, "libgmlp.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "gmlp.h")
+
+PATH_AUTO, PATH_GEMV, PATH_MFMA = 0, 1, 2
+_PATHS = {"auto": PATH_AUTO, "gemv": PATH_GEMV, "mfma": PATH_MFMA}
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "gmlp_version": ([], ctypes.c_int),
+    "gmlp_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "gmlp_last_error": ([], ctypes.c_char_p),
+    "gmlp_validate": ([_I64, _I64, _I64, _P, _P, _P, _P, _P], ctypes.c_int),
+    "gmlp_workspace_size": ([_I64, _I64, _I64], _SZ),
+    "gmlp_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
+    "gmlp_forward": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "gmlp_forward_ws": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
+    "gmlp_forward_ex": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
+                        ctypes.c_int),
+    "gmlp_gate_up": ([_P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "gmlp_down": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+}
+
+_lib = None
+
+
+class GmlpError(RuntimeError):
+    def __init__(self, code: int, detail: str):
+        self.code = code
+        super().__init__("%s: %s" % (status_string(code), detail))
+
+
+def library() -> ctypes.CDLL:
+    """The loaded libgmlp.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBRARY):
+            raise RuntimeError("libgmlp.so is not built: run `python -m paper_2606_26344_amd.build`")
+        lib = ctypes.CDLL(LIBRARY)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = lib
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions include/gmlp.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gmlp_[a-z_0-9]+)\s*\(", text)))
+
+
+def version() -> int:
+    return library().gmlp_version()
+
+
+def status_string(code: int) -> str:
+    return library().gmlp_status_string(code).decode()
+
+
+def last_error() -> str:
+    return library().gmlp_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise GmlpError(rc, last_error())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _expect(t: torch.Tensor, name: str, shape, device) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != torch.bfloat16:
+        raise TypeError("%s must be torch.bfloat16, got %s" % (name, t.dtype))
+    if t.device.type != "cuda" or (device is not None and t.device != device):
+        raise ValueError("%s must be on the HIP device %s, got %s" % (name, device, t.device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+
+
+def workspace_size(T: int, D: int, F: int) -> int:
+    return int(library().gmlp_workspace_size(T, D, F))
+
+
+class Workspace:
+    """A caller-owned workspace for forward(), zeroed once at creation."""
+
+    def __init__(self, T: int, D: int, F: int, device=None, stream=None):
+        n = workspace_size(T, D, F)
+        if n == 0:
+            raise ValueError("invalid shape T=%d D=%d F=%d" % (T, D, F))
+        # 256 bytes of slack so the buffer can be 256-byte aligned.
+        self.storage = torch.empty(n + 256, dtype=torch.uint8, device=device or "cuda")
+        off = (-self.storage.data_ptr()) % 256
+        self.buffer = self.storage[off:off + n]
+        self.nbytes = n
+        _check(library().gmlp_workspace_init(_ptr(self.buffer), n, _stream(stream)))
+
+    def fits(self, T: int, D: int, F: int) -> bool:
+        return workspace_size(T, D, F) <= self.nbytes
+
+
+def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tensor,
+            out: Optional[torch.Tensor] = None, path: str = "auto",
+            workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """Y = (silu(x wg) * (x wu)) wd on the current HIP stream."""
+    if x.dim() != 2 or wg.dim() != 2:
+        raise ValueError("x and wg must be 2-D")
+    T, D = x.shape
+    F = wg.shape[1]
+    dev = x.device
+    _expect(x, "x", (T, D), dev)
+    _expect(wg, "wg", (D, F), dev)
+    _expect(wu, "wu", (D, F), dev)
+    _expect(wd, "wd", (F, D), dev)
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+    _expect(out, "out", (T, D), dev)
+    lib = library()
+    st = _stream(stream)
+    if workspace is None and path == "auto":
+        _check(lib.gmlp_forward(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F, st))
+        return out
+    if workspace is None:
+        workspace = Workspace(T, D, F, device=dev, stream=stream)
+    _check(lib.gmlp_forward_ex(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
+                               _PATHS[path], _ptr(workspace.buffer), workspace.nbytes, st))
+    return out
+
+
+def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
+            out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """H = bf16(silu(x wg) * (x wu)), H [T, F]."""
+    T, D = x.shape
+    F = wg.shape[1]
+    dev = x.device
+    _expect(x, "x", (T, D), dev)
+    _expect(wg, "wg", (D, F), dev)
+    _expect(wu, "wu", (D, F), dev)
+    if out is None:
+        out = torch.empty((T, F), dtype=torch.bfloat16, device=dev)
+    _expect(out, "out", (T, F), dev)
+    _check(library().gmlp_gate_up(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F, _stream(stream)))
+    return out
+
+
+def down(h: torch.Tensor, wd: torch.Tensor, out: Optional[torch.Tensor] = None,
+         stream=None) -> torch.Tensor:
+    """Y = bf16(h wd), h [T, F], wd [F, D]."""
+    T, F = h.shape
+    D = wd.shape[1]
+    dev = h.device
+    _expect(h, "h", (T, F), dev)
+    _expect(wd, "wd", (F, D), dev)
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+    _expect(out, "out", (T, D), dev)
+    _check(library().gmlp_down(_ptr(h), _ptr(wd), _ptr(out), T, F, D, _stream(stream)))
+    return out
+
+
+def from_bf16_bits(bits, device="cuda") -> torch.Tensor:
+    """A bfloat16 device tensor holding the given uint16 bit patterns (numpy)."""
+    import numpy as np
+
+    arr = np.ascontiguousarray(bits, dtype=np.uint16)
+    return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def to_bf16_bits(t: torch.Tensor):
+    """uint16 numpy array of a bfloat16 tensor's bit patterns."""
+    import numpy as np
+
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)

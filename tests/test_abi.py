@@ -1,0 +1,98 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/gmlp.h declares, and rejects bad arguments before touching
+any device (validation runs first and makes no HIP call)."""
+import ctypes
+
+import pytest
+
+from paper_2606_26344_amd import gmlp
+
+A = 0x10000000  # fake, 256-byte aligned addresses: validation never dereferences
+MB = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return gmlp.library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = gmlp.header_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(gmlp._SIGNATURES)
+
+
+def test_version_and_status_strings(lib):
+    assert gmlp.version() == 100
+    assert gmlp.status_string(0) == "GMLP_OK"
+    assert gmlp.status_string(1) == "GMLP_ERR_INVALID_ARG"
+    assert gmlp.status_string(2) == "GMLP_ERR_UNSUPPORTED"
+    assert gmlp.status_string(3) == "GMLP_ERR_HIP"
+    assert gmlp.status_string(4) == "GMLP_ERR_NO_MEMORY"
+    assert gmlp.status_string(99) == "GMLP_ERR_UNKNOWN"
+
+
+def _validate(lib, T, D, F, X=A, Wg=A + 64 * MB, Wu=A + 128 * MB, Wd=A + 192 * MB, Y=A + 256 * MB):
+    return lib.gmlp_validate(T, D, F, X, Wg, Wu, Wd, Y)
+
+
+def test_validate_accepts_good_arguments(lib):
+    assert _validate(lib, 16, 256, 512) == 0
+    assert gmlp.last_error() == ""
+    assert _validate(lib, 0, 8, 8, X=None, Y=None) == 0  # no rows: X, Y may be NULL
+
+
+@pytest.mark.parametrize("T,D,F,code", [
+    (-1, 256, 512, 1), (4, 0, 512, 1), (4, 256, 0, 1), (4, -8, 512, 1),
+    (4, 260, 512, 2), (4, 256, 516, 2), (4, 1 << 23, 8, 2), (1 << 31, 8, 8, 2),
+])
+def test_validate_rejects_bad_shapes(lib, T, D, F, code):
+    assert _validate(lib, T, D, F) == code
+    assert gmlp.last_error() != ""
+
+
+@pytest.mark.parametrize("which", ["X", "Wg", "Wu", "Wd", "Y"])
+def test_validate_rejects_null_and_misaligned(lib, which):
+    assert _validate(lib, 4, 256, 512, **{which: None}) == 1
+    assert _validate(lib, 4, 256, 512, **{which: A + 8}) == 2
+    assert which in gmlp.last_error()
+
+
+def test_validate_rejects_aliasing_output(lib):
+    assert _validate(lib, 4, 256, 512, Y=A) == 1  # Y on top of X
+    assert _validate(lib, 4, 256, 512, Y=A + 64 * MB + 1024) == 1  # inside Wg
+    assert "overlap" in gmlp.last_error()
+
+
+def test_workspace_size(lib):
+    assert gmlp.workspace_size(16, 256, 512) > 0
+    assert gmlp.workspace_size(4096, 4096, 14336) >= 4096 * 14336 * 2  # holds H
+    assert gmlp.workspace_size(1, 4096, 14336) > 0
+    assert gmlp.workspace_size(-1, 256, 512) == 0
+    assert gmlp.workspace_size(4, 260, 512) == 0
+
+
+def test_zero_tokens_is_a_no_op(lib):
+    assert lib.gmlp_forward(None, A, A + 64 * MB, A + 128 * MB, None, 0, 256, 512, None) == 0
+    assert lib.gmlp_forward_ex(None, A, A + 64 * MB, A + 128 * MB, None, 0, 256, 512, 0,
+                               None, 0, None) == 0
+
+
+def test_forward_ex_checks_path_and_workspace_before_launching(lib):
+    args = (A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, 16, 256, 512)
+    n = gmlp.workspace_size(16, 256, 512)
+    assert lib.gmlp_forward_ex(*args, 7, A + 300 * MB, n, None) == 1  # unknown path
+    assert lib.gmlp_forward_ex(*args, gmlp.PATH_GEMV, A + 300 * MB, n, None) == 2  # T > 8
+    assert lib.gmlp_forward_ex(*args, 0, None, n, None) == 1  # no workspace
+    assert lib.gmlp_forward_ex(*args, 0, A + 300 * MB + 16, n, None) == 2  # misaligned
+    assert lib.gmlp_forward_ex(*args, 0, A + 300 * MB, n - 1, None) == 4  # too small
+    assert lib.gmlp_workspace_init(None, 1024, None) == 1
+
+
+def test_helpers_validate_too(lib):
+    assert lib.gmlp_gate_up(A, A + 64 * MB, A + 128 * MB, None, 4, 256, 512, None) == 1
+    assert lib.gmlp_gate_up(A, A + 64 * MB, A + 128 * MB, A, 4, 256, 512, None) == 1  # H on X
+    assert lib.gmlp_down(A, A + 64 * MB, None, 4, 512, 256, None) == 1
+    assert lib.gmlp_down(A, A + 64 * MB, A + 8, 4, 512, 256, None) == 2

@@ -1,0 +1,195 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU fp64 oracle.
+
+Acceptance per output element: |Y_gpu - Y_ref| <= 1e-2 * (|Y_ref| + rms(Y_ref)),
+rms over the checked elements, for bf16 inputs with fp32 accumulation.  The
+same rule is applied to H for the gate/up step alone.  Shapes that the oracle
+can finish in seconds are checked in full; the full-size workloads are
+checked on sampled rows (rows are independent: the oracle computes exactly
+those rows), in the same launch configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_26344_amd import gmlp
+from paper_2606_26344_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def _dev(bits):
+    return gmlp.from_bf16_bits(bits)
+
+
+def _check(got_bits, ref, what=""):
+    got = I.bf16_bits_to_f32(got_bits).astype(np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), "non-finite output " + what
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    bound = TOL * (np.abs(ref) + rms)
+    err = np.abs(got - ref)
+    ratio = float(np.max(err / bound)) if err.size else 0.0
+    print("%s max err/bound = %.3f (rms ref %.4g)" % (what, ratio, rms), flush=True)
+    assert np.all(err <= bound), "%s: %d elements out of tolerance, worst ratio %.3f" % (
+        what, int(np.sum(err > bound)), ratio)
+    return ratio
+
+
+def _run(T, D, F, seed=0, path="auto", rows=None, unit_rms=False, orc=None):
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=seed, unit_rms_rows=unit_rms)
+    x, wg, wu, wd = (_dev(a) for a in (X, Wg, Wu, Wd))
+    ws = gmlp.Workspace(T, D, F)
+    y = gmlp.forward(x, wg, wu, wd, path=path, workspace=ws)
+    torch.cuda.synchronize()
+    Y = gmlp.to_bf16_bits(y)
+    if rows is None:
+        rows = np.arange(T)
+    ref = orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows)
+    return _check(Y[rows], ref, "T=%d D=%d F=%d path=%s" % (T, D, F, path))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    gmlp.library()  # fails loudly when libgmlp.so is missing
+
+
+def test_tiny_workload(orc):
+    w = I.WORKLOADS["tiny"]
+    _run(w.T, w.D, w.F, seed=w.seed, orc=orc)
+
+
+# Ragged shapes: T, D, F not multiples of the tile sizes (D, F multiples of
+# 8), both paths and every tile configuration.
+RAGGED = [
+    (1, 256, 512), (2, 264, 520), (3, 520, 264), (4, 256, 1032), (5, 264, 264),
+    (7, 256, 1032), (8, 264, 264), (9, 256, 512), (15, 264, 520), (16, 520, 1032),
+    (17, 520, 1032), (33, 72, 136), (127, 256, 520), (128, 264, 1032), (129, 520, 264),
+    (255, 256, 264), (257, 264, 520), (300, 1032, 2056),
+]
+
+
+@pytest.mark.parametrize("T,D,F", RAGGED, ids=["T%dD%dF%d" % s for s in RAGGED])
+def test_ragged_shapes(orc, T, D, F):
+    _run(T, D, F, seed=T + D + F, orc=orc)
+
+
+@pytest.mark.parametrize("T", [1, 2, 5, 8])
+def test_small_T_on_the_mfma_path(orc, T):
+    _run(T, 264, 520, seed=40 + T, path="mfma", orc=orc)
+
+
+@pytest.mark.parametrize("T", [1, 3, 8])
+def test_gemv_path_explicitly(orc, T):
+    _run(T, 4104, 2056, seed=50 + T, path="gemv", orc=orc)
+
+
+def test_large_gate_up_tiles_ragged(orc):
+    # 4 x 129 = 516 tiles of 256 x 128: the large gate/up configuration, with
+    # ragged T, D (K tail of 8) and F (a partial 128-column tile).
+    T, D, F = 1000, 264, 16392
+    _run(T, D, F, seed=7, rows=I.sample_rows(T, 96), orc=orc)
+
+
+def test_large_down_tiles_ragged(orc):
+    # 16 x 13 = 208 tiles of 256 x 256: the large down configuration.
+    T, D, F = 4000, 3080, 264
+    _run(T, D, F, seed=8, rows=I.sample_rows(T, 64), orc=orc)
+
+
+def test_gate_up_alone_matches_oracle_h(orc):
+    for T, D, F in [(16, 256, 512), (5, 264, 1032), (200, 520, 264)]:
+        X, Wg, Wu, Wd = I.generate(T, D, F, seed=3)
+        h = gmlp.gate_up(_dev(X), _dev(Wg), _dev(Wu))
+        torch.cuda.synchronize()
+        _, H_ref = orc.gated_mlp_rows(X, Wg, Wu, Wd, return_h=True)
+        _check(gmlp.to_bf16_bits(h), H_ref, "H T=%d D=%d F=%d" % (T, D, F))
+
+
+def test_down_alone_matches_oracle(orc):
+    for T, F, D in [(16, 512, 256), (3, 1032, 264), (130, 264, 520)]:
+        rng = np.random.default_rng(T)
+        H = I.f32_to_bf16_bits(rng.standard_normal((T, F)).astype(np.float32))
+        Wd = I.f32_to_bf16_bits((rng.standard_normal((F, D)) / np.sqrt(F)).astype(np.float32))
+        y = gmlp.down(_dev(H), _dev(Wd))
+        torch.cuda.synchronize()
+        _check(gmlp.to_bf16_bits(y), orc.down_rows(H, Wd), "down T=%d F=%d D=%d" % (T, F, D))
+
+
+def test_forward_without_workspace_allocates_its_own(orc):
+    X, Wg, Wu, Wd = I.generate(12, 256, 520, seed=9)
+    y = gmlp.forward(_dev(X), _dev(Wg), _dev(Wu), _dev(Wd))
+    torch.cuda.synchronize()
+    _check(gmlp.to_bf16_bits(y), orc.gated_mlp_rows(X, Wg, Wu, Wd), "allocating entry")
+
+
+def test_zero_tokens_leaves_output_untouched():
+    X, Wg, Wu, Wd = I.generate(1, 256, 512, seed=0)
+    y = torch.full((1, 256), 3.0, dtype=torch.bfloat16, device="cuda")
+    x0 = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    y0 = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    gmlp.forward(x0, _dev(Wg), _dev(Wu), _dev(Wd), out=y0)
+    torch.cuda.synchronize()
+    assert torch.all(y == 3.0)
+
+
+@pytest.mark.parametrize("T,D,F", [(1, 4096, 14336), (64, 1032, 2056), (600, 512, 4104)])
+def test_bitwise_deterministic(T, D, F):
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=11)
+    args = [_dev(a) for a in (X, Wg, Wu, Wd)]
+    ws = gmlp.Workspace(T, D, F)
+    a = gmlp.forward(*args, workspace=ws).clone()
+    b = gmlp.forward(*args, workspace=ws).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("T", [3, 100, 1000])
+def test_guard_bands_untouched(orc, T):
+    """Writes stay inside Y: canary rows before and after it survive."""
+    D, F = 264, 1032
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=12)
+    pad = 7
+    big = torch.full((T + 2 * pad, D), -77.0, dtype=torch.bfloat16, device="cuda")
+    y = big[pad:pad + T]
+    ws = gmlp.Workspace(T, D, F)
+    gmlp.forward(*[_dev(a) for a in (X, Wg, Wu, Wd)], out=y, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.all(big[:pad] == -77.0) and torch.all(big[pad + T:] == -77.0)
+    _check(gmlp.to_bf16_bits(y), orc.gated_mlp_rows(X, Wg, Wu, Wd), "guarded T=%d" % T)
+
+
+def test_non_default_stream_and_ordering(orc):
+    T, D, F = 40, 520, 1032
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=13)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        args = [_dev(a) for a in (X, Wg, Wu, Wd)]
+        x = args[0] * 1.0  # work queued ahead of the call on the same stream
+        y = gmlp.forward(x, *args[1:], stream=s)
+        z = y.float() * 2.0  # work queued behind it
+    s.synchronize()
+    _check(gmlp.to_bf16_bits(y), orc.gated_mlp_rows(X, Wg, Wu, Wd), "side stream")
+    assert torch.equal(z, y.float() * 2.0)
+
+
+def test_workspace_reused_across_shapes(orc):
+    ws = gmlp.Workspace(300, 1032, 2056)
+    for T, D, F in [(300, 1032, 2056), (4, 1032, 2056), (100, 520, 1032), (1, 264, 264)]:
+        assert ws.fits(T, D, F)
+        X, Wg, Wu, Wd = I.generate(T, D, F, seed=T)
+        y = gmlp.forward(*[_dev(a) for a in (X, Wg, Wu, Wd)], workspace=ws)
+        torch.cuda.synchronize()
+        _check(gmlp.to_bf16_bits(y), orc.gated_mlp_rows(X, Wg, Wu, Wd), "reuse T=%d" % T)
+
+
+# ---- the five workloads at their full sizes ---------------------------------
+
+@pytest.mark.parametrize("name,nrows", [("decode", None), ("small_batch", None),
+                                        ("prefill", 64), ("large_prefill", 48)])
+def test_full_size_workload(orc, name, nrows):
+    w = I.WORKLOADS[name]
+    rows = None if nrows is None else I.sample_rows(w.T, nrows)
+    _run(w.T, w.D, w.F, seed=w.seed, rows=rows, unit_rms=w.unit_rms_rows, orc=orc)

@@ -240,6 +240,22 @@ def pin_bf16_path_matches_f64_path(orc):
     assert np.array_equal(a, b)
 
 
+def pin_down_step_alone(orc):
+    """The down projection alone: one-hot rows of H select rows of Wd, and
+    random bf16 data agrees with numpy's matmul."""
+    from paper_2606_26344_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+
+    F, D = 24, 16
+    Wd = f32_to_bf16_bits(_rng(11).standard_normal((F, D)).astype(np.float32))
+    eye = f32_to_bf16_bits(np.eye(F, dtype=np.float32))
+    got = orc.down_rows(eye, Wd)
+    assert np.array_equal(got, bf16_bits_to_f32(Wd).astype(np.float64))
+    H = f32_to_bf16_bits(_rng(12).standard_normal((5, F)).astype(np.float32))
+    want = bf16_bits_to_f32(H).astype(np.float64) @ bf16_bits_to_f32(Wd).astype(np.float64)
+    ok, worst = _close(orc.down_rows(H, Wd, rows=[4, 1]), want[[4, 1]], 1e-13, 1e-14)
+    assert ok, worst
+
+
 PINS = [
     pin_silu_zero,
     pin_silu_logit_points,
@@ -255,6 +271,7 @@ PINS = [
     pin_library_composite,
     pin_golden_logq,
     pin_bf16_path_matches_f64_path,
+    pin_down_step_alone,
 ]
 
 
