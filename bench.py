@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X SiLU Gated MLP, Y = (silu(X Wg) * (X Wu)) Wd.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one full pass of the hot path (gate/up kernel + down kernel)
+over one batch of synthetic inputs already resident in HBM.  W untimed steps,
+then exactly K steps timed with HIP events on the library's stream,
+bracketed by device synchronisation (the paper times 100 runs after 20
+warm-ups, Section 6.1; those are the defaults here).
+
+Memory-bound workloads rotate through several device copies of the weights
+(over 1 GB in total), so that each step streams its weights from HBM rather
+than from the 256 MB Infinity Cache.
+
+Prints one JSON line per workload (the default workload is the T=1 decode
+shape) with:
+  value      whole-job throughput: GB/s of algorithmic bytes 2(3DF + 2TD)
+             for memory-bound shapes, TFLOP/s of 6TDF for compute-bound ones;
+  roofline   the dominant (gate/up) kernel timed on its own with HIP events:
+             its algorithmic bytes or flops per launch over its average
+             duration, against the MI355X peak (8 TB/s HBM, 2.5 PFLOP/s
+             dense bf16);
+  cpu_baseline  the CPU fp64 oracle on this host's cores, on a bounded
+             sample of the same workload, scaled to the same unit.
+Only one GPU is used: --gpus above 1 exits with a message.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+METRIC = ("Gated-MLP TFLOP/s & % bf16 MFMA peak (prefill); "
+          "GB/s & % HBM peak (decode)")
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (no sparsity)
+RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)  # ~312 FLOP/B
+MALL_DEFEAT_BYTES = 1.1e9      # rotate weights over at least this many bytes
+
+
+def parse_args(argv=None):
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="decode",
+                   help="decode | tiny | small_batch | prefill | large_prefill | all")
+    p.add_argument("--copies", type=int, default=0,
+                   help="weight copies to rotate through (0: enough to exceed 1.1 GB "
+                        "for memory-bound shapes, 1 otherwise)")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="approximate CPU time budget of the oracle baseline")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args(argv)
+
+
+def algorithmic(T, D, F):
+    """Bytes any method must move (X, three weights, Y) and FLOPs (6TDF)."""
+    return 2.0 * (3.0 * D * F + 2.0 * T * D), 6.0 * T * D * F
+
+
+def gate_up_algorithmic(T, D, F):
+    """Per launch of the gate/up kernel: reads X, Wg, Wu, writes H."""
+    return 2.0 * (2.0 * D * F + T * D + T * F), 4.0 * T * D * F
+
+
+def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s):
+    import numpy as np
+
+    import oracle
+
+    orc = oracle.default_oracle()
+    T, D, F = w.T, w.D, w.F
+    nbytes, flops = algorithmic(T, D, F)
+    threads = orc.max_threads()
+    # Calibrate on one row, then size the sample to fill the time budget.
+    t0 = time.perf_counter()
+    orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=[0])
+    t_row = max(time.perf_counter() - t0, 1e-6)
+    n = int(max(1, min(T, budget_s // t_row)))
+    rows = np.linspace(0, T - 1, n).round().astype(np.int64) if n < T else None
+    reps = 1 if n < T else int(max(1, min(1000, budget_s // (t_row * T))))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows)
+    t_total = time.perf_counter() - t0
+    rows_done = (T if rows is None else n)
+    t_full = (t_total / reps) * T / rows_done  # seconds per full step
+    if bound == "hbm":
+        value, unit = nbytes / t_full / 1e9, "GB/s"
+    else:
+        value, unit = flops / t_full / 1e12, "TFLOP/s"
+    if rows is None:
+        sample = "all %d rows, %d repetitions (%.1f s)" % (T, reps, t_total)
+    else:
+        sample = ("%d of %d rows (evenly spaced), %d repetition(s) in %.1f s, "
+                  "time extrapolated x%.1f to the full step" % (n, T, reps, t_total, T / n))
+    return {"value": round(value, 6), "unit": unit, "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds_per_step": t_full}
+
+
+def run_workload(name, args):
+    import torch
+
+    from paper_2606_26344_amd import gmlp
+    from paper_2606_26344_amd import inputs as I
+
+    w = I.WORKLOADS[name]
+    T, D, F = w.T, w.D, w.F
+    nbytes, flops = algorithmic(T, D, F)
+    bound = "hbm" if flops / nbytes < RIDGE else "mfma"
+    lib = gmlp.library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t_gen = time.perf_counter()
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=w.seed, unit_rms_rows=w.unit_rms_rows)
+    t_gen = time.perf_counter() - t_gen
+
+    weight_bytes = 2.0 * 3 * D * F
+    copies = args.copies or (max(3, math.ceil(MALL_DEFEAT_BYTES / weight_bytes))
+                             if bound == "hbm" else 1)
+    x = gmlp.from_bf16_bits(X, dev)
+    wsets = [tuple(gmlp.from_bf16_bits(a, dev) for a in (Wg, Wu, Wd))]
+    for _ in range(copies - 1):
+        wsets.append(tuple(t.clone() for t in wsets[0]))
+    y = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+    h = torch.empty((T, F), dtype=torch.bfloat16, device=dev)
+    ws = gmlp.Workspace(T, D, F, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    P = ctypes.c_void_p
+    xp, yp, hp, wsp = P(x.data_ptr()), P(y.data_ptr()), P(h.data_ptr()), P(ws.buffer.data_ptr())
+    wp = [tuple(P(t.data_ptr()) for t in s) for s in wsets]
+    auto = gmlp.PATH_AUTO
+
+    def step(i):
+        g, u, d = wp[i % copies]
+        return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, auto, wsp, ws.nbytes, st)
+
+    def gate_up_only(i):
+        g, u, _ = wp[i % copies]
+        return lib.gmlp_gate_up_ws(xp, g, u, hp, T, D, F, auto, wsp, ws.nbytes, st)
+
+    def down_only(i):
+        _, _, d = wp[i % copies]
+        return lib.gmlp_down_ws(hp, d, yp, T, F, D, auto, wsp, ws.nbytes, st)
+
+    def timed(fn, k):
+        """Average ms per call over k calls on the library stream (HIP events)."""
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for i in range(k):
+            rc = fn(i)
+            if rc:
+                raise gmlp.GmlpError(rc, gmlp.last_error())
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / k
+
+    # Warm-up, then the timed region: exactly K steps.
+    for i in range(args.warmup):
+        if step(i):
+            raise gmlp.GmlpError(1, gmlp.last_error())
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ms_per_step = timed(step, args.steps)
+    wall = time.perf_counter() - wall0
+
+    # The dominant kernel (gate/up) and the down kernel, each timed alone.
+    k_kernel = max(args.steps, 20)
+    gate_up_ms = timed(gate_up_only, k_kernel)
+    down_ms = timed(down_only, k_kernel)
+
+    sec = ms_per_step / 1e3
+    if bound == "hbm":
+        value, unit = nbytes / sec / 1e9, "GB/s"
+    else:
+        value, unit = flops / sec / 1e12, "TFLOP/s"
+    gu_bytes, gu_flops = gate_up_algorithmic(T, D, F)
+    if bound == "hbm":
+        achieved, peak, r_unit = gu_bytes / (gate_up_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved, peak, r_unit = gu_flops / (gate_up_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+    path = "gemv" if T <= 8 else "mfma"
+    props = torch.cuda.get_device_properties(dev)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: T=%d, D=%d, F=%d%s" % (
+                name, T, D, F, ", X rows at unit RMS" if w.unit_rms_rows else ""),
+            "T": T, "D": D, "F": F,
+            "path": path,
+            "weight_copies_rotated": copies,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": bound,
+            "achieved": round(achieved, 3),
+            "peak": peak,
+            "unit": r_unit,
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+            "kernel": "gate/up (%s)" % ("gemv_splitk_kernel" if path == "gemv" else "gemm_mfma_kernel"),
+            "per_launch": ("%.4g bytes" % gu_bytes) if bound == "hbm" else ("%.4g flop" % gu_flops),
+            "avg_launch_us": round(gate_up_ms * 1e3, 3),
+        },
+        "step": {
+            "gbs": round(nbytes / sec / 1e9, 3),
+            "tflops": round(flops / sec / 1e12, 3),
+            "frac_hbm_peak": round(nbytes / sec / 1e9 / HBM_PEAK_GBS, 4),
+            "frac_bf16_peak": round(flops / sec / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "gate_up_us": round(gate_up_ms * 1e3, 3),
+            "down_us": round(down_ms * 1e3, 3),
+            "wall_s": round(wall, 4),
+        },
+        "device": {"name": props.name, "cus": props.multi_processor_count,
+                   "arch": getattr(props, "gcnArchName", "")},
+        "input_generation_s": round(t_gen, 2),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds)
+    del wsets, x, y, h, ws
+    torch.cuda.empty_cache()
+    return result
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the Gated MLP here runs on a single MI355X "
+              "(--gpus %d, WORLD_SIZE %d requested); run with --gpus 1." % (args.gpus, world),
+              file=sys.stderr)
+        return 2
+    from paper_2606_26344_amd import inputs as I
+
+    names = list(I.WORKLOADS) if args.workload == "all" else [args.workload]
+    for name in names:
+        if name not in I.WORKLOADS:
+            print("unknown workload %r" % name, file=sys.stderr)
+            return 2
+    for name in names:
+        print(json.dumps(run_workload(name, args)), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

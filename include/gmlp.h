@@ -133,6 +133,20 @@ int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t
 int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D,
               void *stream);
 
+/*
+ * gmlp_gate_up and gmlp_down with the kernel path chosen explicitly (enum
+ * gmlp_path) and a caller-provided workspace sized by
+ * gmlp_workspace_size(T, D, F) and prepared by gmlp_workspace_init (its H
+ * region is not used: H is the caller's).  Allocate nothing; each enqueues
+ * exactly one kernel.  gmlp_forward_ex equals gmlp_gate_up_ws into the
+ * workspace's H followed by gmlp_down_ws.
+ */
+int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T,
+                    int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes,
+                    void *stream);
+int gmlp_down_ws(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D,
+                 int path, void *workspace, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -308,6 +308,10 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     }(std::make_integer_sequence<int, STAGES - 1>{});
 
     // ---- split-K: fixed-order reduction by the last block of each tile ----------
+    // Partial sums go out with device-coherent stores; after they complete
+    // (vmcnt 0) the block counts itself in, and the last block of the tile
+    // reads every split's partials with device-coherent loads and adds them
+    // in split order.  No cache-wide write-back or invalidate is needed.
     if (SPLIT && p.splits > 1) {
         const size_t plane = (size_t)N * M;
         float *mine = p.partial + (size_t)split * NW * plane;
@@ -322,22 +326,23 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                         const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
                         const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
                         if (t < N && f < M) {
-                            f32x4 v = {acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
-                                       acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
-                            *(f32x4 *)(mine + w * plane + (size_t)t * M + f) = v;
+                            float *dst = mine + w * plane + (size_t)t * M + f;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                __hip_atomic_store(dst + e, acc[w][mi][ni][4 * j + e], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
                         }
                     }
-        __threadfence();
+        wait_vmcnt<0>();
         __syncthreads();
         if (tid == 0) {
             const uint32_t before =
-                __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             s_last = before == (uint32_t)(p.splits - 1);
         }
         __syncthreads();
         if (!s_last)
             return;
-        __threadfence();
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
@@ -351,22 +356,19 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                         const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
                         const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
                         if (t < N && f < M) {
-                            f32x4 sum = {};
-                            for (int s = 0; s < p.splits; ++s) {
-                                f32x4 v;
-                                if (s == split)
-                                    v = f32x4{acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
-                                              acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
-                                else
-                                    v = __builtin_nontemporal_load(
-                                        (const f32x4 *)(p.partial + ((size_t)s * NW + w) * plane +
-                                                        (size_t)t * M + f));
-                                sum = s == 0 ? v : sum + v;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                float sum = 0.0f;
+                                for (int s = 0; s < p.splits; ++s) {
+                                    const float v =
+                                        s == split ? acc[w][mi][ni][4 * j + e]
+                                                   : __hip_atomic_load(p.partial + ((size_t)s * NW + w) * plane +
+                                                                           (size_t)t * M + f + e,
+                                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                    sum = s == 0 ? v : sum + v;
+                                }
+                                acc[w][mi][ni][4 * j + e] = sum;
                             }
-                            acc[w][mi][ni][4 * j] = sum[0];
-                            acc[w][mi][ni][4 * j + 1] = sum[1];
-                            acc[w][mi][ni][4 * j + 2] = sum[2];
-                            acc[w][mi][ni][4 * j + 3] = sum[3];
                         }
                     }
     }

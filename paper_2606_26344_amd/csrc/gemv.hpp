@@ -8,13 +8,14 @@
 //   * lane (l % 32) owns 8 adjacent columns (one 16-byte load per row); the
 //     two 32-lane halves of a wave and the 4 waves take rows k = g, g+8, ...
 //     (8 row groups), so a wave reads two 512-byte row segments per load
-//     instruction and every lane keeps 2*NW 16-byte loads per unrolled row
-//     pair in flight;
+//     instruction;
 //   * the activations of the slice are staged once in LDS as fp32;
 //   * partial sums are reduced in a fixed order: across the two halves of
 //     the wave by a lane shuffle, across the 4 waves through LDS, and across
 //     the split-K blocks of a strip by the last block to finish (arrival
-//     counter), which adds the per-block sums in split order.
+//     counter), which adds the per-block sums in split order;
+//   * each lane keeps two batches of 16-byte weight loads in flight (the
+//     next batch is issued before the current one is consumed).
 //   The result is therefore bitwise reproducible run to run.
 //
 // The gate/up instantiation (NW = 2) streams Wg and Wu together and its last
@@ -43,11 +44,16 @@ constexpr int kGemvStrip = 256;        // weight columns per block
 constexpr int kGemvMaxSplitRows = 512; // rows of one split (bounds the LDS copy of act)
 constexpr int kGemvThreads = 256;
 
+// Weight rows per lane per load batch: 2*NW*U loads of 16 bytes in flight
+// per lane, double-buffered, within the register budget of NT tokens.
+template <int NT>
+constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : 4; }
+
 template <int NT, int NW, int EPI>
 __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
 {
     constexpr int RG = 8; // row groups per block
-    constexpr int U = 4;  // rows per lane per unrolled step
+    constexpr int U = gemv_batch_rows<NT>();
     __shared__ float xs[NT][kGemvMaxSplitRows];
     __shared__ float red[4][NW][NT][kGemvStrip];
     __shared__ int s_last;
@@ -85,7 +91,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
         wp[0] = p.w0 + (size_t)kb * M + m0 + col;
         if constexpr (NW == 2)
             wp[1] = p.w1 + (size_t)kb * M + m0 + col;
-        auto fma_row = [&](const u32x4 (&v)[NW], int r) {
+        auto fma_row = [&](const u32x4 (&v)[NW], int r) __attribute__((always_inline)) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const float x = xs[t][r];
@@ -98,19 +104,34 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
                     }
             }
         };
-        int r = rg;
-        for (; r + RG * (U - 1) < nrows; r += RG * U) {
-            u32x4 v[U][NW];
+        // Batch b covers rows rg + 8*(b*U + u), u < U.  Every lane of the
+        // block has the same number nb of full batches.
+        auto load_batch = [&](u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
                 for (int w = 0; w < NW; ++w)
-                    v[u][w] = *(const u32x4 *)(wp[w] + (size_t)(r + RG * u) * M);
+                    v[u][w] = *(const u32x4 *)(wp[w] + (size_t)(rg + RG * (b * U + u)) * M);
+        };
+        auto fma_batch = [&](const u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                fma_row(v[u], r + RG * u);
+                fma_row(v[u], rg + RG * (b * U + u));
+        };
+        const int nb = nrows / (RG * U);
+        u32x4 va[U][NW], vb[U][NW];
+        if (nb > 0)
+            load_batch(va, 0);
+        for (int b = 0; b < nb; b += 2) {
+            if (b + 1 < nb)
+                load_batch(vb, b + 1);
+            fma_batch(va, b);
+            if (b + 2 < nb)
+                load_batch(va, b + 2);
+            if (b + 1 < nb)
+                fma_batch(vb, b + 1);
         }
-        for (; r < nrows; r += RG) {
+        for (int r = nb * RG * U + rg; r < nrows; r += RG) {
             u32x4 v[NW];
 #pragma unroll
             for (int w = 0; w < NW; ++w)
@@ -151,24 +172,28 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
             v[w][t] = ((red[0][w][t][tid] + red[1][w][t][tid]) + red[2][w][t][tid]) + red[3][w][t][tid];
 
     if (p.splits > 1) {
+        // Per-block sums go out with device-coherent stores; once they have
+        // completed (vmcnt 0) the block counts itself in.  The block that
+        // arrives last reads every split's sums with device-coherent loads.
+        // No cache-wide write-back or invalidate is needed.
         if (mvalid) {
 #pragma unroll
             for (int w = 0; w < NW; ++w)
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
-                    p.partial[(((size_t)split * NW + w) * NT + t) * M + m] = v[w][t];
+                    __hip_atomic_store(&p.partial[(((size_t)split * NW + w) * NT + t) * M + m], v[w][t],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        __threadfence();
+        wait_vmcnt<0>();
         __syncthreads();
         if (tid == 0) {
             const uint32_t before =
-                __hip_atomic_fetch_add(p.counters + strip, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(p.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             s_last = before == (uint32_t)(p.splits - 1);
         }
         __syncthreads();
         if (!s_last)
             return;
-        __threadfence();
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (mvalid) {
@@ -180,8 +205,9 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
                     for (int sp = 0; sp < p.splits; ++sp) {
                         const float x = sp == split
                                             ? v[w][t]
-                                            : __builtin_nontemporal_load(
-                                                  &p.partial[(((size_t)sp * NW + w) * NT + t) * M + m]);
+                                            : __hip_atomic_load(
+                                                  &p.partial[(((size_t)sp * NW + w) * NT + t) * M + m],
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         s = sp == 0 ? x : s + x;
                     }
                     v[w][t] = s;

@@ -123,9 +123,10 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.N = N;
     s.K = K;
     s.strips = (int)cdiv(M, kGemvStrip);
-    // About four blocks per CU, split rows a multiple of 8, at most the LDS copy.
+    // About four blocks per CU; split rows a multiple of 64 (whole load
+    // batches for every lane), at most the LDS copy of the activations.
     int64_t splits = std::max<int64_t>(1, cdiv(1024, s.strips));
-    int64_t per = std::max<int64_t>(8, cdiv(cdiv(K, splits), 8) * 8);
+    int64_t per = std::max<int64_t>(64, cdiv(cdiv(K, splits), 64) * 64);
     per = std::min<int64_t>(per, kGemvMaxSplitRows);
     s.k_split = (int)per;
     s.splits = (int)cdiv(K, per);
@@ -455,8 +456,10 @@ int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, 
     return gmlp_forward_ex(X, Wg, Wu, Wd, Y, T, D, F, GMLP_PATH_AUTO, s.ptr, l.total, stream);
 }
 
-int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
-                 int64_t F, void *stream)
+namespace {
+
+int check_gate_up_args(const void *X, const void *Wg, const void *Wu, const void *H, int64_t T,
+                       int64_t D, int64_t F)
 {
     int rc;
     if ((rc = check_shape(T, D, F)) || (rc = check_ptr(X, "X", T > 0)) ||
@@ -466,19 +469,10 @@ int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t
     const size_t hb = (size_t)T * F * 2, xb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
     if (overlaps(H, hb, X, xb) || overlaps(H, hb, Wg, wb) || overlaps(H, hb, Wu, wb))
         return fail(GMLP_ERR_INVALID_ARG, "H overlaps an input");
-    if (T == 0)
-        return ok();
-    const Layout l = make_layout(T, D, F);
-    const Plan plan = make_plan(T, D, F, GMLP_PATH_AUTO);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    Scratch s;
-    if ((rc = s.alloc(l.total, l, st)) ||
-        (rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(s.ptr), l, st)))
-        return rc;
-    return ok();
+    return GMLP_OK;
 }
 
-int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D, void *stream)
+int check_down_args(const void *H, const void *Wd, const void *Y, int64_t T, int64_t F, int64_t D)
 {
     int rc;
     if ((rc = check_shape(T, D, F)) || (rc = check_ptr(H, "H", T > 0)) ||
@@ -487,16 +481,74 @@ int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int6
     const size_t hb = (size_t)T * F * 2, yb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
     if (overlaps(Y, yb, H, hb) || overlaps(Y, yb, Wd, wb))
         return fail(GMLP_ERR_INVALID_ARG, "Y overlaps an input");
+    return GMLP_OK;
+}
+
+} // namespace
+
+int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
+                    int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+{
+    int rc;
+    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)) || (rc = check_path(path, T)))
+        return rc;
     if (T == 0)
         return ok();
     const Layout l = make_layout(T, D, F);
-    const Plan plan = make_plan(T, D, F, GMLP_PATH_AUTO);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    Scratch s;
-    if ((rc = s.alloc(l.total, l, st)) ||
-        (rc = run_down(plan.down, H, Wd, Y, static_cast<uint8_t *>(s.ptr), l, st)))
+    if ((rc = check_workspace(workspace, ws_bytes, l)))
+        return rc;
+    const Plan plan = make_plan(T, D, F, path);
+    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(workspace), l,
+                          static_cast<hipStream_t>(stream))))
         return rc;
     return ok();
+}
+
+int gmlp_down_ws(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D, int path,
+                 void *workspace, size_t ws_bytes, void *stream)
+{
+    int rc;
+    if ((rc = check_down_args(H, Wd, Y, T, F, D)) || (rc = check_path(path, T)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    if ((rc = check_workspace(workspace, ws_bytes, l)))
+        return rc;
+    const Plan plan = make_plan(T, D, F, path);
+    if ((rc = run_down(plan.down, H, Wd, Y, static_cast<uint8_t *>(workspace), l,
+                       static_cast<hipStream_t>(stream))))
+        return rc;
+    return ok();
+}
+
+int gmlp_gate_up(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
+                 int64_t F, void *stream)
+{
+    int rc;
+    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, static_cast<hipStream_t>(stream))))
+        return rc;
+    return gmlp_gate_up_ws(X, Wg, Wu, H, T, D, F, GMLP_PATH_AUTO, s.ptr, l.total, stream);
+}
+
+int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D, void *stream)
+{
+    int rc;
+    if ((rc = check_down_args(H, Wd, Y, T, F, D)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, static_cast<hipStream_t>(stream))))
+        return rc;
+    return gmlp_down_ws(H, Wd, Y, T, F, D, GMLP_PATH_AUTO, s.ptr, l.total, stream);
 }
 
 } // extern "C"

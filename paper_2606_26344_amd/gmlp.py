@@ -45,6 +45,9 @@ _SIGNATURES = {
                         ctypes.c_int),
     "gmlp_gate_up": ([_P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_down": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
+    "gmlp_gate_up_ws": ([_P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
+                        ctypes.c_int),
+    "gmlp_down_ws": ([_P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P], ctypes.c_int),
 }
 
 _lib = None
@@ -169,7 +172,8 @@ def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tenso
 
 
 def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
-            out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+            out: Optional[torch.Tensor] = None, path: str = "auto",
+            workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
     """H = bf16(silu(x wg) * (x wu)), H [T, F]."""
     T, D = x.shape
     F = wg.shape[1]
@@ -180,12 +184,20 @@ def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
     if out is None:
         out = torch.empty((T, F), dtype=torch.bfloat16, device=dev)
     _expect(out, "out", (T, F), dev)
-    _check(library().gmlp_gate_up(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F, _stream(stream)))
+    if workspace is None and path == "auto":
+        _check(library().gmlp_gate_up(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
+                                      _stream(stream)))
+        return out
+    if workspace is None:
+        workspace = Workspace(T, D, F, device=dev, stream=stream)
+    _check(library().gmlp_gate_up_ws(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
+                                     _PATHS[path], _ptr(workspace.buffer), workspace.nbytes,
+                                     _stream(stream)))
     return out
 
 
 def down(h: torch.Tensor, wd: torch.Tensor, out: Optional[torch.Tensor] = None,
-         stream=None) -> torch.Tensor:
+         path: str = "auto", workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
     """Y = bf16(h wd), h [T, F], wd [F, D]."""
     T, F = h.shape
     D = wd.shape[1]
@@ -195,7 +207,13 @@ def down(h: torch.Tensor, wd: torch.Tensor, out: Optional[torch.Tensor] = None,
     if out is None:
         out = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
     _expect(out, "out", (T, D), dev)
-    _check(library().gmlp_down(_ptr(h), _ptr(wd), _ptr(out), T, F, D, _stream(stream)))
+    if workspace is None and path == "auto":
+        _check(library().gmlp_down(_ptr(h), _ptr(wd), _ptr(out), T, F, D, _stream(stream)))
+        return out
+    if workspace is None:
+        workspace = Workspace(T, D, F, device=dev, stream=stream)
+    _check(library().gmlp_down_ws(_ptr(h), _ptr(wd), _ptr(out), T, F, D, _PATHS[path],
+                                  _ptr(workspace.buffer), workspace.nbytes, _stream(stream)))
     return out
 
 
