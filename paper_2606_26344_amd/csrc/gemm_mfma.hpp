@@ -11,7 +11,7 @@
 //     from the fp32 accumulators; G and U never leave registers.
 //   * down:            NW = 1 (Wd), epilogue writes Y = bf16(H Wd).
 //
-// Data flow per k-step of 64:
+// Data flow per k-step of BK:
 //   global --(buffer_load ... lds, 16 B per lane, zero-filled out of range)-->
 //   LDS (STAGES-deep ring; 16-byte chunks XOR-swizzled so that the fragment
 //   reads below are free of bank conflicts) --> registers --> MFMA.
@@ -31,6 +31,13 @@
 // the row-major [N, M] layout of H and Y and is stored as 8-byte rows
 // without any transpose (the operand swap the paper derives for
 // transpose(nc_matmul(a, b)), Section 4.5).
+//
+// Schedule.  One wave per SIMD holds all accumulators (up to 256 AGPRs).
+// Fragments are double-buffered in VGPRs, and the instruction order inside
+// each k16 step is pinned with scheduling-group barriers: every MFMA is
+// followed by one LDS fragment read for the next step and, in the step that
+// follows a pipeline barrier, by one DMA issue for a future k-tile, so the
+// matrix pipe does not wait on LDS latency or on issuing loads.
 #pragma once
 
 #include <utility>
@@ -47,15 +54,17 @@ struct GemmParams {
     float *partial;      // split-K partial sums [splits][NW][N][M] fp32
     uint32_t *counters;  // split-K arrival counter per output tile (zero on entry and exit)
     int M, N, K;
-    int k_split; // K rows per split (a multiple of 64 when splits > 1)
+    int k_split; // K rows per split (a multiple of BK when splits > 1)
     int splits;
     int tiles_m, tiles_n;
+    int group_m; // consecutive blocks sweep group_m column tiles before the next token tile
 };
 
-template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_>
+template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_, int BK_>
 struct GemmShape {
     static constexpr int NW = NW_, WM = WM_, WN = WN_, TM = TM_, TN = TN_, STAGES = STAGES_;
-    static constexpr int BK = 64;
+    static constexpr int BK = BK_;
+    static constexpr int KSTEPS = BK / 16;         // MFMA k16 steps per k-tile
     static constexpr int NWAVES = WM * WN;
     static constexpr int NTHREADS = NWAVES * 64;
     static constexpr int BMW = WM * TM * 32;       // columns per weight per tile
@@ -63,6 +72,8 @@ struct GemmShape {
     static constexpr int W_ROW_BYTES = BMW * 2;    // one k row of a weight tile
     static constexpr int W_CPR = BMW / 8;          // 16-byte chunks per weight row
     static constexpr int W_TILE_BYTES = BK * BMW * 2;
+    static constexpr int X_ROW_BYTES = BK * 2;     // one token row of an activation tile
+    static constexpr int X_CPR = BK / 8;           // 16-byte chunks per token row
     static constexpr int X_TILE_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = NW * W_TILE_BYTES + X_TILE_BYTES;
     static constexpr int W_LOADS = W_TILE_BYTES / (NTHREADS * 16); // per weight, per thread
@@ -70,10 +81,14 @@ struct GemmShape {
     static constexpr int LOADS_PER_STAGE = NW * W_LOADS + X_LOADS;
     static constexpr int W_LPR = 64 / W_CPR;          // weight rows per wave load
     static constexpr int W_RPI = NWAVES * W_LPR;      // weight rows per load step i
+    static constexpr int X_LPR = 64 / X_CPR;          // token rows per wave load
+    static constexpr int FRAG_READS = NW * TM * 2 + TN;  // LDS reads per k16 step
+    static constexpr int MFMAS = NW * TM * TN;           // MFMAs per k16 step
+    static_assert(BK == 32 || BK == 64, "k-tile of 32 or 64");
     static_assert(BMW >= 64, "weight rows of at least 8 chunks");
     static_assert(W_TILE_BYTES % (NTHREADS * 16) == 0 && X_TILE_BYTES % (NTHREADS * 16) == 0,
                   "every thread issues whole 16-byte loads");
-    static_assert(STAGES >= 2 && STAGES <= 4, "2..4 LDS stages");
+    static_assert(STAGES >= 2 && STAGES <= 5, "2..5 LDS stages");
     static_assert((STAGES - 2) * LOADS_PER_STAGE < 64, "vmcnt range");
     static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS capacity of a CU");
 };
@@ -92,10 +107,40 @@ __device__ __forceinline__ int w_swizzle(int k)
     }
 }
 
-// Physical chunk of logical chunk c (0..7) in token row t of an activation
-// tile: any 8 (and any aligned 16) consecutive rows reading one logical chunk
-// hit distinct banks.
-__device__ __forceinline__ int x_swizzle(int t) { return (t ^ (t >> 3)) & 7; }
+// Physical chunk of logical chunk c in token row t of an activation tile:
+// any 8 (and any aligned 16) consecutive rows reading one logical chunk hit
+// distinct banks, for rows of 8 chunks (128 B) or 4 chunks (64 B).
+template <int CPR>
+__device__ __forceinline__ int x_swizzle(int t)
+{
+    if constexpr (CPR == 8)
+        return (t ^ (t >> 3)) & 7;
+    else
+        return ((t >> 1) ^ (t >> 3)) & 3;
+}
+
+// Pin the instruction order of one k16 step: each MFMA is followed by one
+// global (DMA) load and one LDS read, while any remain.
+template <int N_MFMA, int N_DS, int N_VMEM>
+__device__ __forceinline__ void interleave_step()
+{
+    constexpr int kMFMA = 0x008, kDSRead = 0x100, kVMEMRead = 0x020;
+    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+        (
+            [&] {
+                __builtin_amdgcn_sched_group_barrier(kMFMA, 1, 0);
+                if constexpr (I < N_VMEM)
+                    __builtin_amdgcn_sched_group_barrier(kVMEMRead, 1, 0);
+                if constexpr (I < N_DS)
+                    __builtin_amdgcn_sched_group_barrier(kDSRead, 1, 0);
+            }(),
+            ...);
+    }(std::make_integer_sequence<int, N_MFMA>{});
+    if constexpr (N_DS > N_MFMA)
+        __builtin_amdgcn_sched_group_barrier(kDSRead, N_DS - N_MFMA, 0);
+    if constexpr (N_VMEM > N_MFMA)
+        __builtin_amdgcn_sched_group_barrier(kVMEMRead, N_VMEM - N_MFMA, 0);
+}
 
 // SPLIT selects the split-K variant (several blocks per output tile, summed
 // by the last one); without it p.splits must be 1.
@@ -103,24 +148,36 @@ template <class S, int EPI, bool SPLIT>
 __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
 {
     constexpr int NW = S::NW, TM = S::TM, TN = S::TN, STAGES = S::STAGES;
-    constexpr int NWAVES = S::NWAVES;
+    constexpr int NWAVES = S::NWAVES, KSTEPS = S::KSTEPS;
     // One LDS array per pipeline stage: distinct objects let the compiler see
     // that reading one stage does not depend on the DMA into another.
     __shared__ __attribute__((aligned(1024))) uint8_t lds0[S::STAGE_BYTES];
     __shared__ __attribute__((aligned(1024))) uint8_t lds1[S::STAGE_BYTES];
     __shared__ __attribute__((aligned(1024))) uint8_t lds2[STAGES > 2 ? S::STAGE_BYTES : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t lds3[STAGES > 3 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds4[STAGES > 4 ? S::STAGE_BYTES : 16];
     __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % S::WM, wn = wave / S::WM;
 
+    // Block -> (split, tile).  Each XCD gets a contiguous range of the
+    // order; within it, consecutive blocks sweep group_m column tiles for
+    // one token tile, then the next token tile, so the blocks resident on
+    // one XCD share few distinct weight and activation strips in its L2.
     const int ntiles = p.tiles_m * p.tiles_n;
     const int id = xcd_contiguous_id(blockIdx.x, ntiles * p.splits);
     const int split = id / ntiles;
-    const int tile = id - split * ntiles;
-    const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
+    const int tile_id = id - split * ntiles;
+    const int per_group = p.group_m * p.tiles_n;
+    const int group = tile_id / per_group;
+    const int first_m = group * p.group_m;
+    const int group_w = min(p.tiles_m - first_m, p.group_m);
+    const int in_group = tile_id - group * per_group;
+    const int tm = first_m + in_group % group_w;
+    const int tn = in_group / group_w;
+    const int tile = tm * p.tiles_n + tn; // counter slot for split-K
     const int M = p.M, N = p.N, K = p.K;
     const int m0 = tm * S::BMW, n0 = tn * S::BN;
     const int kb = split * p.k_split;
@@ -132,7 +189,8 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         if constexpr (decltype(s)::value == 0) return lds0;
         else if constexpr (decltype(s)::value == 1) return lds1;
         else if constexpr (decltype(s)::value == 2) return lds2;
-        else return lds3;
+        else if constexpr (decltype(s)::value == 3) return lds3;
+        else return lds4;
     };
 
     // ---- staging addresses ---------------------------------------------------
@@ -150,37 +208,37 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     uint32_t x_voff[S::X_LOADS];
 #pragma unroll
     for (int i = 0; i < S::X_LOADS; ++i) {
-        const int t = (i * NWAVES + wave) * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ x_swizzle(t);
+        const int t = (i * NWAVES + wave) * S::X_LPR + lane / S::X_CPR;
+        const int c = (lane % S::X_CPR) ^ x_swizzle<S::X_CPR>(t);
         x_voff[i] = (uint32_t)((min(n0 + t, N - 1) - n0) * K + c * 8) * 2u;
     }
 
-    // Issue the DMA of k-tile kt into stage buffer sbuf.  Only a partial last
-    // tile needs per-lane k masks (rows of W and columns of act past the end
-    // of the k range read as zeros).
+    // Issue the DMA of k-tile kt into stage buffer sbuf, without branches so
+    // that the loads can be interleaved with MFMAs.  A partial last tile
+    // gets per-lane k masks (rows of W and columns of act past the end of
+    // the k range read as zeros); a tile past the end (kt >= nk) reads only
+    // zeros into a buffer nobody reads again, which keeps the count of loads
+    // in flight the same at every step.
     auto issue = [&](uint8_t *sbuf, int kt) __attribute__((always_inline)) {
         const int k0 = kb + kt * S::BK;
-        const int krem = ke - k0;
-        const bool tail = ragged_k && kt == nk - 1;
+        const int krem = kt < nk ? ke - k0 : 0;
+        const bool masked = ragged_k ? kt >= nk - 1 : kt >= nk;
         const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.act + (size_t)n0 * K + k0);
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
             const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? p.w0 : p.w1) + (size_t)k0 * M + m0);
 #pragma unroll
             for (int i = 0; i < S::W_LOADS; ++i) {
-                const uint32_t v = (tail && i * S::W_RPI + w_k >= krem) ? kOutOfRange : w_voff;
+                const uint32_t v = (masked && i * S::W_RPI + w_k >= krem) ? kOutOfRange : w_voff;
                 load16_to_lds(rw, sbuf + w * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v,
                               (uint32_t)i * w_soff_step);
             }
         }
 #pragma unroll
         for (int i = 0; i < S::X_LOADS; ++i) {
-            uint32_t v = x_voff[i];
-            if (tail) {
-                const int t = (i * NWAVES + wave) * 8 + (lane >> 3);
-                const int c = (lane & 7) ^ x_swizzle(t);
-                v = c * 8 < krem ? v : kOutOfRange;
-            }
+            const int t = (i * NWAVES + wave) * S::X_LPR + lane / S::X_CPR;
+            const int c = (lane % S::X_CPR) ^ x_swizzle<S::X_CPR>(t);
+            const uint32_t v = (masked && c * 8 >= krem) ? kOutOfRange : x_voff[i];
             load16_to_lds(rx, sbuf + NW * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v);
         }
     };
@@ -196,14 +254,15 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         a_off[mi] = r_lane * S::W_ROW_BYTES + ((c ^ w_swizzle<S::W_CPR>(r_lane)) << 4) + (lane & 1) * 8;
     }
     // Token (B) fragment of n-tile ni: row t = wn*TN*32 + ni*32 + lane%32,
-    // logical chunk 2*kk + lane/32.  The row bits of the swizzle differ
-    // between even and odd ni only, and rows are 128 bytes, so the byte
-    // address is (b_base[ni & 1] + ni*4096) ^ (32*kk).
+    // logical chunk 2*kk + lane/32.  n-tiles are 32 rows apart, which leaves
+    // the swizzle unchanged for 64-byte rows and flips it by parity for
+    // 128-byte rows; the chunk bits of the address are XORed with 2*kk.
     int b_base[2];
 #pragma unroll
     for (int par = 0; par < 2; ++par) {
         const int t = wn * TN * 32 + par * 32 + (lane & 31);
-        b_base[par] = t * 128 + ((((lane >> 5) ^ x_swizzle(t))) << 4) - par * 4096;
+        b_base[par] = t * S::X_ROW_BYTES + ((((lane >> 5) ^ x_swizzle<S::X_CPR>(t))) << 4) -
+                      par * 32 * S::X_ROW_BYTES;
     }
 
     f32x16 acc[NW][TM][TN];
@@ -234,7 +293,7 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
             }
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni) {
-            const int off = (b_base[ni & 1] + ni * 4096) ^ (32 * kk);
+            const int off = (b_base[ni & 1] + ni * 32 * S::X_ROW_BYTES) ^ (32 * kk);
             f.b[ni] = *(const bf16x8 *)(sx + off);
         }
     };
@@ -248,54 +307,59 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                     acc[w][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[w][mi], f.b[ni],
                                                                              acc[w][mi][ni], 0, 0, 0);
     };
-    // Tile kt has landed in LDS (for every wave) once at most the tiles
-    // issued after it are in flight and all waves have passed a barrier.
-    auto wait_tile = [&](int kt) __attribute__((always_inline)) {
-        if (kt + STAGES - 2 < nk)
-            wait_vmcnt<(STAGES - 2) * S::LOADS_PER_STAGE>();
-        else
-            wait_vmcnt<0>();
+    // A tile has landed in LDS (for every wave) once at most the STAGES - 2
+    // tiles issued after it are in flight and all waves have passed a
+    // barrier.  Every step issues exactly one tile (real or past the end),
+    // so the count is the same at every step.
+    auto wait_tile = [&]() __attribute__((always_inline)) {
+        wait_vmcnt<(STAGES - 2) * S::LOADS_PER_STAGE>();
         wait_lgkm0();
         barrier_only();
     };
 
     // ---- pipelined main loop -------------------------------------------------
     // Stage buffer of tile kt is kt % STAGES.  Fragments are double-buffered
-    // in registers: the reads for k16 step kk+1 are issued before the MFMAs
-    // of step kk.  At the last step of a tile the next tile's first
-    // fragments are read after the barrier that also frees this tile's
-    // buffer for the DMA of tile kt + STAGES.
+    // in registers: the reads for k16 step kk+1 are issued among the MFMAs of
+    // step kk.  Before the last step of a tile, a barrier makes the next
+    // tile visible and frees this tile's buffer; the DMA of tile kt + STAGES
+    // into it and the next tile's first fragment reads are then issued among
+    // the last step's MFMAs.
+    static_assert(KSTEPS % 2 == 0, "k16 steps alternate between two fragment buffers");
     Frags f0, f1;
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-        ((I < nk ? issue(stage_ptr(std::integral_constant<int, I>{}), I) : void()), ...);
+        (issue(stage_ptr(std::integral_constant<int, I>{}), I), ...);
     }(std::make_integer_sequence<int, STAGES - 1>{});
-    if (nk > 0) {
-        wait_tile(0);
-        if (STAGES - 1 < nk)
-            issue(stage_ptr(std::integral_constant<int, STAGES - 1>{}), STAGES - 1);
-    }
+    wait_tile();
+    issue(stage_ptr(std::integral_constant<int, STAGES - 1>{}), STAGES - 1);
     load_frags(f0, lds0, 0);
 
-    // One k-tile held in stage buffer I.  Only uniform branches around
-    // side-effecting work (waits, DMA issue): the registers flow straight
-    // through, so accumulators and fragments need no copies.  At the last
-    // tile the next-tile fragment read touches stale LDS and is unused.
+    // One k-tile held in stage buffer I, without branches: the registers
+    // flow straight through (accumulators and fragments need no copies) and
+    // each k16 step is one scheduling region.  At the last tile the next-tile
+    // fragment read touches stale LDS and is unused.
     auto step = [&](auto stage, int kt) __attribute__((always_inline)) {
         constexpr int I = decltype(stage)::value;
         uint8_t *buf = stage_ptr(stage);
-        load_frags(f1, buf, 1);
-        mma(f0);
-        load_frags(f0, buf, 2);
-        mma(f1);
-        load_frags(f1, buf, 3);
-        mma(f0);
-        if (kt + 1 < nk) {
-            wait_tile(kt + 1);
-            if (kt + STAGES < nk)
-                issue(buf, kt + STAGES);
-        }
+        [&]<int... KK>(std::integer_sequence<int, KK...>) __attribute__((always_inline)) {
+            (
+                [&] {
+                    // k16 step KK: fragments of step KK+1 among its MFMAs.
+                    if constexpr (KK % 2 == 0) {
+                        load_frags(f1, buf, KK + 1);
+                        mma(f0);
+                    } else {
+                        load_frags(f0, buf, KK + 1);
+                        mma(f1);
+                    }
+                    interleave_step<S::MFMAS, S::FRAG_READS, 0>();
+                }(),
+                ...);
+        }(std::make_integer_sequence<int, KSTEPS - 1>{});
+        wait_tile();
+        issue(buf, kt + STAGES);
         load_frags(f0, stage_ptr(std::integral_constant<int, (I + 1) % STAGES>{}), 0);
         mma(f1);
+        interleave_step<S::MFMAS, S::FRAG_READS, S::LOADS_PER_STAGE>();
     };
     int kt = 0;
     for (; kt + STAGES <= nk; kt += STAGES) {
@@ -306,6 +370,9 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
         ((kt + I < nk ? step(std::integral_constant<int, I>{}, kt + I) : void()), ...);
     }(std::make_integer_sequence<int, STAGES - 1>{});
+    // Drain the loads issued past the end before LDS can be handed to
+    // another block.
+    wait_vmcnt<0>();
 
     // ---- split-K: fixed-order reduction by the last block of each tile ----------
     // Partial sums go out with device-coherent stores; after they complete

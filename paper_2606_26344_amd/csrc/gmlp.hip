@@ -38,11 +38,15 @@ int ok()
 }
 
 // ---- tile configurations -------------------------------------------------
-//                       NW WM WN TM TN STAGES
-using GateUpLarge = GemmShape<2, 2, 2, 2, 4, 2>; // 128 F cols x 256 tokens, per weight
-using GateUpSmall = GemmShape<2, 2, 2, 1, 2, 4>; //  64 F cols x 128 tokens
-using DownLarge = GemmShape<1, 2, 2, 4, 4, 2>;   // 256 D cols x 256 tokens
-using DownSmall = GemmShape<1, 2, 2, 2, 2, 4>;   // 128 D cols x 128 tokens
+//                          NW WM WN TM TN STAGES BK
+using GateUpLarge = GemmShape<2, 2, 2, 2, 4, 3, 32>; // 128 F cols x 256 tokens, per weight
+using GateUpSmall = GemmShape<2, 2, 2, 1, 2, 4, 64>; //  64 F cols x 128 tokens
+using DownLarge = GemmShape<1, 2, 2, 4, 4, 4, 32>;   // 256 D cols x 256 tokens
+using DownSmall = GemmShape<1, 2, 2, 2, 2, 4, 64>;   // 128 D cols x 128 tokens
+// Column tiles swept per token tile by consecutive blocks (L2 locality),
+// from a sweep at T=4096/2048 on MI355X.
+constexpr int kGroupGateUp = 4;
+constexpr int kGroupDown = 8;
 
 constexpr int kGemvMaxTokens = 8;
 constexpr int64_t kMaxDim = int64_t(1) << 22; // D, F: keeps 32-bit tile offsets in range
@@ -64,6 +68,7 @@ struct Step {
     Kind kind = K_NONE;
     int M = 0, N = 0, K = 0;
     int tiles_m = 0, tiles_n = 0; // GEMM
+    int group_m = 1;              // GEMM block order
     int strips = 0;               // GEMV
     int splits = 1, k_split = 0;
     int blocks = 0, threads = 0;
@@ -95,7 +100,7 @@ void choose_splits(Step &s, int tiles, int target, int tile_k, int min_tiles)
 }
 
 template <class S>
-void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split)
+void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split, int group_m)
 {
     s.kind = kind;
     s.M = M;
@@ -103,6 +108,7 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.K = K;
     s.tiles_m = (int)cdiv(M, S::BMW);
     s.tiles_n = (int)cdiv(N, S::BN);
+    s.group_m = std::max(1, std::min(group_m, s.tiles_m));
     const int tiles = s.tiles_m * s.tiles_n;
     if (allow_split)
         choose_splits(s, tiles, 256, S::BK, 2);
@@ -149,13 +155,13 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     }
     // Gate/up: large tiles once there are enough of them to fill the chip.
     if (cdiv(T, GateUpLarge::BN) * cdiv(F, GateUpLarge::BMW) >= 512)
-        gemm_step<GateUpLarge>(p.gate_up, K_GEMM_GU_L, (int)F, (int)T, (int)D, 2, false);
+        gemm_step<GateUpLarge>(p.gate_up, K_GEMM_GU_L, (int)F, (int)T, (int)D, 2, false, kGroupGateUp);
     else
-        gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true);
+        gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
     if (cdiv(T, DownLarge::BN) * cdiv(D, DownLarge::BMW) >= 192)
-        gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false);
+        gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false, kGroupDown);
     else
-        gemm_step<DownSmall>(p.down, K_GEMM_DN_S, (int)D, (int)T, (int)F, 1, true);
+        gemm_step<DownSmall>(p.down, K_GEMM_DN_S, (int)D, (int)T, (int)F, 1, true, kGroupDown);
     return p;
 }
 
@@ -258,6 +264,7 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.splits = s.splits;
     p.tiles_m = s.tiles_m;
     p.tiles_n = s.tiles_n;
+    p.group_m = s.group_m;
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
     hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
