@@ -72,8 +72,12 @@ struct GemmShape {
     static constexpr int W_ROW_BYTES = BMW * 2;    // one k row of a weight tile
     static constexpr int W_CPR = BMW / 8;          // 16-byte chunks per weight row
     static constexpr int W_TILE_BYTES = BK * BMW * 2;
-    static constexpr int X_ROW_BYTES = BK * 2;     // one token row of an activation tile
-    static constexpr int X_CPR = BK / 8;           // 16-byte chunks per token row
+    // Activation tiles are stored as 128-byte LDS rows of 8 chunks.  With
+    // BK = 32 one token row is 4 chunks, so row r holds token r in chunks
+    // 0..3 and token r + BN/2 in chunks 4..7.
+    static constexpr int X_HALVES = 128 / (BK * 2); // tokens per 128-byte LDS row
+    static constexpr int X_ROWS = BN / X_HALVES;    // LDS rows of an activation tile
+    static constexpr int X_CPT = BK / 8;            // 16-byte chunks per token
     static constexpr int X_TILE_BYTES = BN * BK * 2;
     static constexpr int STAGE_BYTES = NW * W_TILE_BYTES + X_TILE_BYTES;
     static constexpr int W_LOADS = W_TILE_BYTES / (NTHREADS * 16); // per weight, per thread
@@ -81,10 +85,10 @@ struct GemmShape {
     static constexpr int LOADS_PER_STAGE = NW * W_LOADS + X_LOADS;
     static constexpr int W_LPR = 64 / W_CPR;          // weight rows per wave load
     static constexpr int W_RPI = NWAVES * W_LPR;      // weight rows per load step i
-    static constexpr int X_LPR = 64 / X_CPR;          // token rows per wave load
     static constexpr int FRAG_READS = NW * TM * 2 + TN;  // LDS reads per k16 step
     static constexpr int MFMAS = NW * TM * TN;           // MFMAs per k16 step
     static_assert(BK == 32 || BK == 64, "k-tile of 32 or 64");
+    static_assert(X_ROWS % 32 == 0, "n-tiles of 32 tokens do not straddle the two row halves");
     static_assert(BMW >= 64, "weight rows of at least 8 chunks");
     static_assert(W_TILE_BYTES % (NTHREADS * 16) == 0 && X_TILE_BYTES % (NTHREADS * 16) == 0,
                   "every thread issues whole 16-byte loads");
@@ -107,17 +111,10 @@ __device__ __forceinline__ int w_swizzle(int k)
     }
 }
 
-// Physical chunk of logical chunk c in token row t of an activation tile:
-// any 8 (and any aligned 16) consecutive rows reading one logical chunk hit
-// distinct banks, for rows of 8 chunks (128 B) or 4 chunks (64 B).
-template <int CPR>
-__device__ __forceinline__ int x_swizzle(int t)
-{
-    if constexpr (CPR == 8)
-        return (t ^ (t >> 3)) & 7;
-    else
-        return ((t >> 1) ^ (t >> 3)) & 3;
-}
+// Physical chunk of logical chunk c in LDS row r of an activation tile
+// (rows of 8 chunks): any 8, and any aligned 16, consecutive rows reading
+// one logical chunk hit distinct banks.
+__device__ __forceinline__ int x_swizzle(int r) { return (r ^ (r >> 3)) & 7; }
 
 // Pin the instruction order of one k16 step: each MFMA is followed by one
 // global (DMA) load and one LDS read, while any remain.
@@ -203,13 +200,18 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     const bool w_col_ok = m0 + w_c * 8 < M;
     const uint32_t w_voff = w_col_ok ? (uint32_t)(w_k * M + w_c * 8) * 2u : kOutOfRange;
     const uint32_t w_soff_step = (uint32_t)S::W_RPI * (uint32_t)M * 2u;
-    // Activation load i: token row x_t(i), chunk x_c(i).  Rows past N are
+    // Activation load i: LDS row x_r(i) (8 rows per wave load), physical
+    // chunk lane % 8 holding chunk x_c of token x_t.  Tokens past N are
     // clamped to N-1: they only feed output rows that are never stored.
     uint32_t x_voff[S::X_LOADS];
+    int x_kcol[S::X_LOADS];
 #pragma unroll
     for (int i = 0; i < S::X_LOADS; ++i) {
-        const int t = (i * NWAVES + wave) * S::X_LPR + lane / S::X_CPR;
-        const int c = (lane % S::X_CPR) ^ x_swizzle<S::X_CPR>(t);
+        const int r = (i * NWAVES + wave) * 8 + (lane >> 3);
+        const int cc = (lane & 7) ^ x_swizzle(r);
+        const int t = r + (cc / S::X_CPT) * S::X_ROWS;
+        const int c = cc % S::X_CPT;
+        x_kcol[i] = c * 8;
         x_voff[i] = (uint32_t)((min(n0 + t, N - 1) - n0) * K + c * 8) * 2u;
     }
 
@@ -236,9 +238,7 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         }
 #pragma unroll
         for (int i = 0; i < S::X_LOADS; ++i) {
-            const int t = (i * NWAVES + wave) * S::X_LPR + lane / S::X_CPR;
-            const int c = (lane % S::X_CPR) ^ x_swizzle<S::X_CPR>(t);
-            const uint32_t v = (masked && c * 8 >= krem) ? kOutOfRange : x_voff[i];
+            const uint32_t v = (masked && x_kcol[i] >= krem) ? kOutOfRange : x_voff[i];
             load16_to_lds(rx, sbuf + NW * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v);
         }
     };
@@ -253,16 +253,17 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         const int c = wm * TM * 4 + mi * 4 + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
         a_off[mi] = r_lane * S::W_ROW_BYTES + ((c ^ w_swizzle<S::W_CPR>(r_lane)) << 4) + (lane & 1) * 8;
     }
-    // Token (B) fragment of n-tile ni: row t = wn*TN*32 + ni*32 + lane%32,
-    // logical chunk 2*kk + lane/32.  n-tiles are 32 rows apart, which leaves
-    // the swizzle unchanged for 64-byte rows and flips it by parity for
-    // 128-byte rows; the chunk bits of the address are XORed with 2*kk.
-    int b_base[2];
+    // Token (B) fragment of n-tile ni: token t = wn*TN*32 + ni*32 + lane%32,
+    // logical chunk 2*kk + lane/32 of that token, i.e. LDS row t % X_ROWS,
+    // combined chunk 2*kk + lane/32 + X_CPT * (t / X_ROWS).  The chunk bits
+    // of the byte address are XORed with 32*kk for step kk.
+    int b_off[TN];
 #pragma unroll
-    for (int par = 0; par < 2; ++par) {
-        const int t = wn * TN * 32 + par * 32 + (lane & 31);
-        b_base[par] = t * S::X_ROW_BYTES + ((((lane >> 5) ^ x_swizzle<S::X_CPR>(t))) << 4) -
-                      par * 32 * S::X_ROW_BYTES;
+    for (int ni = 0; ni < TN; ++ni) {
+        const int t = wn * TN * 32 + ni * 32 + (lane & 31);
+        const int r = t % S::X_ROWS;
+        const int cc = (lane >> 5) + S::X_CPT * (t / S::X_ROWS);
+        b_off[ni] = r * 128 + ((cc ^ x_swizzle(r)) << 4);
     }
 
     f32x16 acc[NW][TM][TN];
@@ -292,10 +293,8 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                 f.a[w][mi] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
             }
 #pragma unroll
-        for (int ni = 0; ni < TN; ++ni) {
-            const int off = (b_base[ni & 1] + ni * 32 * S::X_ROW_BYTES) ^ (32 * kk);
-            f.b[ni] = *(const bf16x8 *)(sx + off);
-        }
+        for (int ni = 0; ni < TN; ++ni)
+            f.b[ni] = *(const bf16x8 *)(sx + (b_off[ni] ^ (32 * kk)));
     };
     auto mma = [&](const Frags &f) __attribute__((always_inline)) {
 #pragma unroll
