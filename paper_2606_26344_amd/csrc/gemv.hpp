@@ -3,7 +3,7 @@
 // With T <= 8 every weight byte is used for at most 8 multiply-adds, so the
 // matmuls of the Gated MLP (Fig. fig:mlp-example, Section 4.1) are bound by
 // the rate at which the weights stream from HBM.  Each block streams a strip
-// of 256 weight columns over a slice of k rows:
+// of up to 256 weight columns over a slice of k rows:
 //
 //   * lane (l % 32) owns 8 adjacent columns (one 16-byte load per row); the
 //     two 32-lane halves of a wave and the 4 waves take rows k = g, g+8, ...
@@ -35,36 +35,70 @@ struct GemvParams {
     float *partial;      // [splits][NW][NT][M] fp32 per-block sums
     uint32_t *counters;  // arrival counter per strip (zero on entry and exit)
     int M, K;
-    int k_split; // rows per split, <= kGemvMaxSplitRows
+    int k_split;     // rows per split, <= gemv_max_split_rows<NT>()
     int splits;
     int strips;
+    int strip_lanes; // lanes per row (8 columns each, <= 32): strip width 8 * strip_lanes
 };
 
-constexpr int kGemvStrip = 256;        // weight columns per block
-constexpr int kGemvMaxSplitRows = 512; // rows of one split (bounds the LDS copy of act)
+constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
 constexpr int kGemvThreads = 256;
 
 // Weight rows per lane per load batch: 2*NW*U loads of 16 bytes in flight
-// per lane, double-buffered, within the register budget of NT tokens.
+// per lane (two batches), within the register budget of NT tokens.
+template <int NT, int NW>
+constexpr int gemv_batch_rows() { return NT <= 2 ? (NW == 1 ? 16 : 8) : 4; }
+
+// Rows of one split: the split's activations are staged in LDS as fp32
+// (NT x rows floats, at most 16 KB).
 template <int NT>
-constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : 4; }
+constexpr int gemv_max_split_rows() { return NT <= 2 ? 2048 : 4096 / NT; }
 
 template <int NT, int NW, int EPI>
 __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
 {
     constexpr int RG = 8; // row groups per block
-    constexpr int U = gemv_batch_rows<NT>();
-    __shared__ float xs[NT][kGemvMaxSplitRows];
-    __shared__ float red[4][NW][NT][kGemvStrip];
+    constexpr int U = gemv_batch_rows<NT, NW>();
+    __shared__ float xs[NT][gemv_max_split_rows<NT>()];
+    __shared__ float red[4][NW][NT][kGemvMaxStrip];
     __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int strip = blockIdx.x % p.strips;
     const int split = blockIdx.x / p.strips;
     const int M = p.M, K = p.K;
-    const int m0 = strip * kGemvStrip;
+    const int width = 8 * p.strip_lanes;
+    const int m0 = strip * width;
     const int kb = split * p.k_split;
     const int nrows = min(K, kb + p.k_split) - kb;
+
+    const int col = (lane & 31) * 8;
+    const int rg = wave * 2 + (lane >> 5);
+    const bool valid = (lane & 31) < p.strip_lanes && m0 + col < M;
+
+    // Weight rows of batch b: rg + 8*(b*U + u), u < U; every lane of the
+    // block runs the same nb batches, the last of which may be partial
+    // (rows past the split are neither loaded nor accumulated).  The loads
+    // bypass caching (each weight byte is read once).
+    const uint16_t *wp[NW];
+    wp[0] = p.w0 + (size_t)kb * M + m0 + col;
+    if constexpr (NW == 2)
+        wp[1] = p.w1 + (size_t)kb * M + m0 + col;
+    auto load_batch = [&](u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int r = rg + RG * (b * U + u);
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                v[u][w] = r < nrows ? __builtin_nontemporal_load((const u32x4 *)(wp[w] + (size_t)r * M))
+                                    : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    const int nb = (nrows + RG * U - 1) / (RG * U);
+    u32x4 va[U][NW], vb[U][NW];
+    // The first weight batch is in flight while the activations are staged.
+    if (valid && nb > 0)
+        load_batch(va, 0);
 
     // Stage this slice of the activations as fp32.
     for (int i = tid; i < NT * nrows; i += kGemvThreads) {
@@ -72,10 +106,6 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
         xs[t][r] = __builtin_bit_cast(float, (uint32_t)p.act[(size_t)t * K + kb + r] << 16);
     }
     __syncthreads();
-
-    const int col = (lane & 31) * 8;
-    const int rg = wave * 2 + (lane >> 5);
-    const bool valid = m0 + col < M;
 
     float acc[NW][NT][8];
 #pragma unroll
@@ -87,10 +117,6 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
                 acc[w][t][e] = 0.0f;
 
     if (valid) {
-        const uint16_t *wp[NW];
-        wp[0] = p.w0 + (size_t)kb * M + m0 + col;
-        if constexpr (NW == 2)
-            wp[1] = p.w1 + (size_t)kb * M + m0 + col;
         auto fma_row = [&](const u32x4 (&v)[NW], int r) __attribute__((always_inline)) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
@@ -104,24 +130,14 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
                     }
             }
         };
-        // Batch b covers rows rg + 8*(b*U + u), u < U.  Every lane of the
-        // block has the same number nb of full batches.
-        auto load_batch = [&](u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int w = 0; w < NW; ++w)
-                    v[u][w] = *(const u32x4 *)(wp[w] + (size_t)(rg + RG * (b * U + u)) * M);
-        };
         auto fma_batch = [&](const u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                fma_row(v[u], rg + RG * (b * U + u));
+            for (int u = 0; u < U; ++u) {
+                const int r = rg + RG * (b * U + u);
+                if (r < nrows)
+                    fma_row(v[u], r);
+            }
         };
-        const int nb = nrows / (RG * U);
-        u32x4 va[U][NW], vb[U][NW];
-        if (nb > 0)
-            load_batch(va, 0);
         for (int b = 0; b < nb; b += 2) {
             if (b + 1 < nb)
                 load_batch(vb, b + 1);
@@ -130,13 +146,6 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
                 load_batch(va, b + 2);
             if (b + 1 < nb)
                 fma_batch(vb, b + 1);
-        }
-        for (int r = nb * RG * U + rg; r < nrows; r += RG) {
-            u32x4 v[NW];
-#pragma unroll
-            for (int w = 0; w < NW; ++w)
-                v[w] = *(const u32x4 *)(wp[w] + (size_t)r * M);
-            fma_row(v, r);
         }
     }
 
@@ -163,7 +172,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
 
     // Thread tid now owns column m0 + tid of the strip.
     const int m = m0 + tid;
-    const bool mvalid = m < M;
+    const bool mvalid = tid < width && m < M;
     float v[NW][NT];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
@@ -197,18 +206,32 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (mvalid) {
+            // Sum the splits in order 0, 1, 2, ...; loads are issued eight
+            // at a time so their latencies overlap.
+            constexpr int B = 8;
 #pragma unroll
             for (int w = 0; w < NW; ++w)
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
+                    const float own = v[w][t];
+                    const float *src = &p.partial[((size_t)w * NT + t) * M + m];
+                    const size_t stride = (size_t)NW * NT * M;
                     float s = 0.0f;
-                    for (int sp = 0; sp < p.splits; ++sp) {
-                        const float x = sp == split
-                                            ? v[w][t]
-                                            : __hip_atomic_load(
-                                                  &p.partial[(((size_t)sp * NW + w) * NT + t) * M + m],
-                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        s = sp == 0 ? x : s + x;
+                    for (int s0 = 0; s0 < p.splits; s0 += B) {
+                        float x[B];
+#pragma unroll
+                        for (int u = 0; u < B; ++u) {
+                            const int sp = s0 + u;
+                            x[u] = sp == split ? own
+                                   : sp < p.splits
+                                       ? __hip_atomic_load(src + sp * stride, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                       : 0.0f;
+                        }
+#pragma unroll
+                        for (int u = 0; u < B; ++u)
+                            if (s0 + u < p.splits)
+                                s = s0 + u == 0 ? x[u] : s + x[u];
                     }
                     v[w][t] = s;
                 }

@@ -70,6 +70,7 @@ struct Step {
     int tiles_m = 0, tiles_n = 0; // GEMM
     int group_m = 1;              // GEMM block order
     int strips = 0;               // GEMV
+    int strip_lanes = 32;         // GEMV: 8-column lanes per row
     int splits = 1, k_split = 0;
     int blocks = 0, threads = 0;
     size_t partial_bytes = 0; // fp32 split-K partial sums
@@ -122,22 +123,63 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
 }
 
+template <int NT>
+constexpr int gemv_rows_limit()
+{
+    return gemv_max_split_rows<NT>();
+}
+
+int gemv_max_rows(int nt)
+{
+    switch (nt) {
+    case 1: return gemv_rows_limit<1>();
+    case 2: return gemv_rows_limit<2>();
+    case 3: return gemv_rows_limit<3>();
+    case 4: return gemv_rows_limit<4>();
+    case 5: return gemv_rows_limit<5>();
+    case 6: return gemv_rows_limit<6>();
+    case 7: return gemv_rows_limit<7>();
+    default: return gemv_rows_limit<8>();
+    }
+}
+
+// Rows one GEMV lane streams per load batch, times the 8 row groups.
+int gemv_batch_span(int nt, int nw)
+{
+    return 8 * (nt <= 2 ? (nw == 1 ? gemv_batch_rows<1, 1>() : gemv_batch_rows<1, 2>())
+                        : gemv_batch_rows<8, 2>());
+}
+
+// GEMV decomposition: strips of 256 columns (32 lanes x 8) times k splits.
+// The kernels are bound by HBM, not by any one CU, so blocks need not be
+// spread evenly over CUs; what matters is enough blocks (and loads) in
+// flight, equal splits of whole load batches, and few splits (each adds a
+// partial sum to the final reduction).  Measured on MI355X at D=4096,
+// F=14336: about 400-500 blocks, splits of whole batches.
 void gemv_step(Step &s, int M, int N, int K, int nw)
 {
     s.kind = K_GEMV;
     s.M = M;
     s.N = N;
     s.K = K;
-    s.strips = (int)cdiv(M, kGemvStrip);
-    // About four blocks per CU; split rows a multiple of 64 (whole load
-    // batches for every lane), at most the LDS copy of the activations.
-    int64_t splits = std::max<int64_t>(1, cdiv(1024, s.strips));
-    int64_t per = std::max<int64_t>(64, cdiv(cdiv(K, splits), 64) * 64);
-    per = std::min<int64_t>(per, kGemvMaxSplitRows);
-    s.k_split = (int)per;
-    s.splits = (int)cdiv(K, per);
-    s.blocks = s.strips * s.splits;
     s.threads = kGemvThreads;
+    s.strip_lanes = 32;
+    s.strips = (int)cdiv(M, 8 * s.strip_lanes);
+    const int max_rows = gemv_max_rows(N);
+    const int span = gemv_batch_span(N, nw);
+    const int64_t lo = std::max<int64_t>(cdiv(K, max_rows), cdiv(384, s.strips));
+    const int64_t hi = std::max<int64_t>(lo, cdiv(K, span));
+    int64_t rows = 0;
+    for (int64_t sp = lo; sp <= std::min<int64_t>(hi, 4 * lo) && !rows; ++sp)
+        if (K % sp == 0 && (K / sp) % span == 0 && K / sp <= max_rows)
+            rows = K / sp; // equal splits of whole batches
+    if (!rows) {
+        const int64_t sp = std::min(lo, hi);
+        rows = std::min<int64_t>(max_rows, cdiv(cdiv(K, sp), span) * span);
+    }
+    s.k_split = (int)rows;
+    s.splits = (int)cdiv(K, rows);
+    s.blocks = s.strips * s.splits;
     s.counters = s.splits > 1 ? s.strips : 0;
     s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
 }
@@ -287,6 +329,7 @@ int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *ac
     p.k_split = s.k_split;
     p.splits = s.splits;
     p.strips = s.strips;
+    p.strip_lanes = s.strip_lanes;
     hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI>), dim3(s.blocks), dim3(kGemvThreads), 0,
                        stream, p);
     return hip_check(hipGetLastError(), "GEMV launch");
