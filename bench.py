@@ -41,6 +41,37 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (no sparsity)
 RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)  # ~312 FLOP/B
 MALL_DEFEAT_BYTES = 1.1e9      # rotate weights over at least this many bytes
+COPY_BYTES = 256 << 20         # size of the calibration copy
+HERE = os.path.dirname(os.path.abspath(__file__))
+PROFILES = os.path.join(HERE, "profiles")
+CSRC = os.path.join(HERE, "paper_2606_26344_amd", "csrc")
+
+
+def kernel_source_sha256():
+    """Hash of the HIP sources: a traffic record is only valid for the
+    kernels it was measured on."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".hpp")):
+            with open(os.path.join(CSRC, name), "rb") as fh:
+                h.update(name.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def committed_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 record
+    for this workload, or None if absent or measured on other sources."""
+    path = os.path.join(PROFILES, "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != kernel_source_sha256():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("traffic_bytes_per_launch")
 
 
 def parse_args(argv=None):
@@ -56,6 +87,16 @@ def parse_args(argv=None):
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="approximate CPU time budget of the oracle baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="after the timed region, run plain device copies of %d MiB (a known "
+                        "number of bytes) for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE"
+                        % (COPY_BYTES >> 20))
+    p.add_argument("--summarize-profile", metavar="DIR", nargs="+",
+                   help="print per-kernel averages from rocprofv3 CSV output directories "
+                        "and exit (no GPU work)")
+    p.add_argument("--write-traffic", metavar="JSON",
+                   help="with --summarize-profile: FETCH_SIZE and WRITE_SIZE runs of "
+                        "--copy-calibration benches -> traffic record for the roofline")
     return p.parse_args(argv)
 
 
@@ -84,7 +125,7 @@ def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s):
     t_row = max(time.perf_counter() - t0, 1e-6)
     n = int(max(1, min(T, budget_s // t_row)))
     rows = np.linspace(0, T - 1, n).round().astype(np.int64) if n < T else None
-    reps = 1 if n < T else int(max(1, min(1000, budget_s // (t_row * T))))
+    reps = 1 if n < T else int(max(1, min(100000, budget_s // (t_row * T))))
     t0 = time.perf_counter()
     for _ in range(reps):
         orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows)
@@ -190,6 +231,7 @@ def run_workload(name, args):
     else:
         achieved, peak, r_unit = gu_flops / (gate_up_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
     path = "gemv" if T <= 8 else "mfma"
+    gate_up_kernel = "gemv_splitk_kernel<%d, 2, 0>" % T if path == "gemv" else "gemm_mfma_kernel (gate/up)"
     props = torch.cuda.get_device_properties(dev)
     result = {
         "metric": METRIC,
@@ -218,8 +260,8 @@ def run_workload(name, args):
             "peak": peak,
             "unit": r_unit,
             "frac": round(achieved / peak, 4),
-            "traffic": None,
-            "kernel": "gate/up (%s)" % ("gemv_splitk_kernel" if path == "gemv" else "gemm_mfma_kernel"),
+            "traffic": committed_traffic(name, gate_up_kernel),
+            "kernel": gate_up_kernel,
             "per_launch": ("%.4g bytes" % gu_bytes) if bound == "hbm" else ("%.4g flop" % gu_flops),
             "avg_launch_us": round(gate_up_ms * 1e3, 3),
         },
@@ -236,6 +278,16 @@ def run_workload(name, args):
                    "arch": getattr(props, "gcnArchName", "")},
         "input_generation_s": round(t_gen, 2),
     }
+    if args.copy_calibration:
+        # A plain elementwise pass reading and writing COPY_BYTES (the only
+        # elementwise kernel this script launches).
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1, out=dst)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = COPY_BYTES
+        del src, dst
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds)
     del wsets, x, y, h, ws
@@ -243,8 +295,78 @@ def run_workload(name, args):
     return result
 
 
+def _read_counter_csvs(dirs):
+    """Per-kernel mean of each counter over dispatches (rocprofv3 CSV)."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    tot = defaultdict(lambda: defaultdict(float))
+    disp = defaultdict(lambda: defaultdict(set))
+    for d in dirs:
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as fh:
+                for r in csv.DictReader(fh):
+                    k, c = r["Kernel_Name"], r["Counter_Name"]
+                    tot[k][c] += float(r["Counter_Value"])
+                    disp[k][c].add((path, r["Dispatch_Id"]))
+    return {k: {c: v / len(disp[k][c]) for c, v in cs.items()} for k, cs in tot.items()}
+
+
+def _read_kernel_stats(dirs):
+    import csv
+    import glob
+
+    rows = []
+    for d in dirs:
+        for path in glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True):
+            with open(path) as fh:
+                rows += list(csv.DictReader(fh))
+    return rows
+
+
+def summarize_profile(args):
+    counters = _read_counter_csvs(args.summarize_profile)
+    for k, cs in sorted(counters.items()):
+        print(k)
+        for c, v in sorted(cs.items()):
+            print("    %-28s %.6g" % (c, v))
+    for r in _read_kernel_stats(args.summarize_profile):
+        print("%-80s calls %6s  avg %10.3f us  total %12.3f us  %6.2f%%" % (
+            r["Name"][:80], r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["TotalDurationNs"]) / 1e3, float(r["Percentage"])))
+    if args.write_traffic:
+        # Calibrate against the plain copy: it reads and writes COPY_BYTES.
+        copy = [cs for k, cs in counters.items() if "elementwise" in k.lower()]
+        fetch_copy = max((cs.get("FETCH_SIZE", 0.0) for cs in copy), default=0.0)
+        write_copy = max((cs.get("WRITE_SIZE", 0.0) for cs in copy), default=0.0)
+        f_fetch = COPY_BYTES / 1024.0 / fetch_copy if fetch_copy else None
+        f_write = COPY_BYTES / 1024.0 / write_copy if write_copy else None
+        rec = {"source_sha256": kernel_source_sha256(), "copy_bytes": COPY_BYTES,
+               "copy_fetch_kib": fetch_copy, "copy_write_kib": write_copy,
+               "fetch_factor": f_fetch, "write_factor": f_write, "kernels": {}}
+        for k, cs in counters.items():
+            if "gemv_splitk_kernel" in k or "gemm_mfma_kernel" in k:
+                short = k.split("(")[0].replace("void gmlp::", "")
+                if "gemm_mfma_kernel" in short:
+                    short = "gemm_mfma_kernel (%s)" % ("gate/up" if "2, 2, 2" in short else "down")
+                fe, wr = cs.get("FETCH_SIZE"), cs.get("WRITE_SIZE")
+                tb = None
+                if fe is not None and wr is not None and f_fetch and f_write:
+                    tb = round(fe * 1024.0 * f_fetch + wr * 1024.0 * f_write)
+                rec["kernels"][short] = {"fetch_kib_per_launch": fe, "write_kib_per_launch": wr,
+                                         "traffic_bytes_per_launch": tb}
+        with open(args.write_traffic, "w") as fh:
+            json.dump(rec, fh, indent=1, sort_keys=True)
+            fh.write("\n")
+        print("wrote", args.write_traffic)
+    return 0
+
+
 def main(argv=None):
     args = parse_args(argv)
+    if args.summarize_profile:
+        return summarize_profile(args)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the Gated MLP here runs on a single MI355X "
