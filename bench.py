@@ -3,8 +3,9 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
-One step is one full pass of the hot path (gate/up kernel + down kernel)
-over one batch of synthetic inputs already resident in HBM.  W untimed steps,
+One step is one full pass of the hot path (one fused persistent GEMV kernel
+for T <= 7, else a gate/up kernel and a down kernel) over one batch of
+synthetic inputs already resident in HBM.  W untimed steps,
 then exactly K steps timed with HIP events on the library's stream,
 bracketed by device synchronisation (the paper times 100 runs after 20
 warm-ups, Section 6.1; those are the defaults here).
@@ -17,10 +18,11 @@ Prints one JSON line per workload (the default workload is the T=1 decode
 shape) with:
   value      whole-job throughput: GB/s of algorithmic bytes 2(3DF + 2TD)
              for memory-bound shapes, TFLOP/s of 6TDF for compute-bound ones;
-  roofline   the dominant (gate/up) kernel timed on its own with HIP events:
-             its algorithmic bytes or flops per launch over its average
-             duration, against the MI355X peak (8 TB/s HBM, 2.5 PFLOP/s
-             dense bf16);
+  roofline   the dominant kernel timed with HIP events on the library's
+             stream (the fused kernel, which is the whole step, or else the
+             gate/up kernel launched on its own): its algorithmic bytes or
+             flops per launch over its average duration, against the MI355X
+             peak (8 TB/s HBM, 2.5 PFLOP/s dense bf16);
   cpu_baseline  the CPU fp64 oracle on this host's cores, on a bounded
              sample of the same workload, scaled to the same unit.
 Only one GPU is used: --gpus above 1 exits with a message.
@@ -215,23 +217,29 @@ def run_workload(name, args):
     ms_per_step = timed(step, args.steps)
     wall = time.perf_counter() - wall0
 
-    # The dominant kernel (gate/up) and the down kernel, each timed alone.
+    # The gate/up and down kernels, each launched and timed alone.
     k_kernel = max(args.steps, 20)
     gate_up_ms = timed(gate_up_only, k_kernel)
     down_ms = timed(down_only, k_kernel)
+    plan = gmlp.describe(T, D, F)
 
     sec = ms_per_step / 1e3
     if bound == "hbm":
         value, unit = nbytes / sec / 1e9, "GB/s"
     else:
         value, unit = flops / sec / 1e12, "TFLOP/s"
-    gu_bytes, gu_flops = gate_up_algorithmic(T, D, F)
-    if bound == "hbm":
-        achieved, peak, r_unit = gu_bytes / (gate_up_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    if len(plan) == 1:
+        # One kernel is the whole step: its launches are the timed steps.
+        dom_kernel, dom_ms = plan[0][0], ms_per_step
+        dom_bytes, dom_flops = nbytes, flops
     else:
-        achieved, peak, r_unit = gu_flops / (gate_up_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+        dom_kernel, dom_ms = plan[0][0], gate_up_ms
+        dom_bytes, dom_flops = gate_up_algorithmic(T, D, F)
+    if bound == "hbm":
+        achieved, peak, r_unit = dom_bytes / (dom_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved, peak, r_unit = dom_flops / (dom_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
     path = "gemv" if T <= 8 else "mfma"
-    gate_up_kernel = "gemv_splitk_kernel<%d, 2, 0>" % T if path == "gemv" else "gemm_mfma_kernel (gate/up)"
     props = torch.cuda.get_device_properties(dev)
     result = {
         "metric": METRIC,
@@ -251,6 +259,7 @@ def run_workload(name, args):
                 name, T, D, F, ", X rows at unit RMS" if w.unit_rms_rows else ""),
             "T": T, "D": D, "F": F,
             "path": path,
+            "kernels": [{"name": k, "grid": g, "block": b, "k_splits": sp} for k, g, b, sp in plan],
             "weight_copies_rotated": copies,
             "parallelism": "single GPU",
         },
@@ -260,18 +269,18 @@ def run_workload(name, args):
             "peak": peak,
             "unit": r_unit,
             "frac": round(achieved / peak, 4),
-            "traffic": committed_traffic(name, gate_up_kernel),
-            "kernel": gate_up_kernel,
-            "per_launch": ("%.4g bytes" % gu_bytes) if bound == "hbm" else ("%.4g flop" % gu_flops),
-            "avg_launch_us": round(gate_up_ms * 1e3, 3),
+            "traffic": committed_traffic(name, dom_kernel),
+            "kernel": dom_kernel,
+            "per_launch": ("%.4g bytes" % dom_bytes) if bound == "hbm" else ("%.4g flop" % dom_flops),
+            "avg_launch_us": round(dom_ms * 1e3, 3),
         },
         "step": {
             "gbs": round(nbytes / sec / 1e9, 3),
             "tflops": round(flops / sec / 1e12, 3),
             "frac_hbm_peak": round(nbytes / sec / 1e9 / HBM_PEAK_GBS, 4),
             "frac_bf16_peak": round(flops / sec / 1e12 / BF16_PEAK_TFLOPS, 4),
-            "gate_up_us": round(gate_up_ms * 1e3, 3),
-            "down_us": round(down_ms * 1e3, 3),
+            "gate_up_alone_us": round(gate_up_ms * 1e3, 3),
+            "down_alone_us": round(down_ms * 1e3, 3),
             "wall_s": round(wall, 4),
         },
         "device": {"name": props.name, "cus": props.multi_processor_count,
@@ -346,10 +355,9 @@ def summarize_profile(args):
                "copy_fetch_kib": fetch_copy, "copy_write_kib": write_copy,
                "fetch_factor": f_fetch, "write_factor": f_write, "kernels": {}}
         for k, cs in counters.items():
-            if "gemv_splitk_kernel" in k or "gemm_mfma_kernel" in k:
-                short = k.split("(")[0].replace("void gmlp::", "")
-                if "gemm_mfma_kernel" in short:
-                    short = "gemm_mfma_kernel (%s)" % ("gate/up" if "2, 2, 2" in short else "down")
+            if "gmlp::" in k:
+                # The name gmlp_describe gives the kernel.
+                short = k.split("(gmlp::")[0].replace("void ", "", 1).replace("gmlp::", "")
                 fe, wr = cs.get("FETCH_SIZE"), cs.get("WRITE_SIZE")
                 tb = None
                 if fe is not None and wr is not None and f_fetch and f_write:

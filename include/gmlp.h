@@ -84,6 +84,17 @@ int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg
                   const void *Wu, const void *Wd, const void *Y);
 
 /*
+ * The kernels gmlp_forward_ex(..., path, ...) enqueues for this shape, as
+ * text: one line per kernel, in launch order,
+ *     "<kernel> grid=<blocks> block=<threads> k_splits=<n>\n"
+ * with <kernel> as a profiler names it without the namespace (for example
+ * "gemv_splitk_kernel<1, 2, 0>").  NUL-terminated, truncated to `bytes`
+ * (which must be > 0).  Host-only: makes no HIP call.  Nothing for T == 0.
+ * GMLP_OK, or INVALID_ARG / UNSUPPORTED for a bad shape, path or buffer.
+ */
+int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t bytes);
+
+/*
  * Bytes of workspace gmlp_forward_ws / gmlp_forward_ex need for this shape
  * (for any path).  The workspace holds H [T, F] bf16, fp32 split-K partial
  * sums and a block of arrival counters.  0 if the shape is invalid.
@@ -138,8 +149,8 @@ int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int6
  * gmlp_path) and a caller-provided workspace sized by
  * gmlp_workspace_size(T, D, F) and prepared by gmlp_workspace_init (its H
  * region is not used: H is the caller's).  Allocate nothing; each enqueues
- * exactly one kernel.  gmlp_forward_ex equals gmlp_gate_up_ws into the
- * workspace's H followed by gmlp_down_ws.
+ * exactly one kernel.  gmlp_forward_ex gives the same bits as gmlp_gate_up_ws
+ * into the workspace's H followed by gmlp_down_ws.
  */
 int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T,
                     int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes,

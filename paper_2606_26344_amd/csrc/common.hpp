@@ -27,6 +27,10 @@ constexpr int kRawBufferWord3 = 0x00020000;
 // range and return zeros (used to zero-fill tile edges).
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kNumRecords = 0x7fffffff;
+// Cache-policy operand of the buffer load/store builtins for device-coherent
+// (agent-scope) accesses on gfx950: the SC1 bit, the same policy the compiler
+// gives agent-scope atomic loads and stores.
+constexpr int kCoherent = 16;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base)
 {

@@ -92,7 +92,7 @@ struct GemmShape {
     static_assert(BMW >= 64, "weight rows of at least 8 chunks");
     static_assert(W_TILE_BYTES % (NTHREADS * 16) == 0 && X_TILE_BYTES % (NTHREADS * 16) == 0,
                   "every thread issues whole 16-byte loads");
-    static_assert(STAGES >= 2 && STAGES <= 5, "2..5 LDS stages");
+    static_assert(STAGES >= 2 && STAGES <= 8, "2..8 LDS stages");
     static_assert((STAGES - 2) * LOADS_PER_STAGE < 64, "vmcnt range");
     static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS capacity of a CU");
 };
@@ -153,6 +153,9 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     __shared__ __attribute__((aligned(1024))) uint8_t lds2[STAGES > 2 ? S::STAGE_BYTES : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t lds3[STAGES > 3 ? S::STAGE_BYTES : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t lds4[STAGES > 4 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds5[STAGES > 5 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds6[STAGES > 6 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds7[STAGES > 7 ? S::STAGE_BYTES : 16];
     __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -187,7 +190,10 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         else if constexpr (decltype(s)::value == 1) return lds1;
         else if constexpr (decltype(s)::value == 2) return lds2;
         else if constexpr (decltype(s)::value == 3) return lds3;
-        else return lds4;
+        else if constexpr (decltype(s)::value == 4) return lds4;
+        else if constexpr (decltype(s)::value == 5) return lds5;
+        else if constexpr (decltype(s)::value == 6) return lds6;
+        else return lds7;
     };
 
     // ---- staging addresses ---------------------------------------------------
@@ -374,31 +380,38 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     wait_vmcnt<0>();
 
     // ---- split-K: fixed-order reduction by the last block of each tile ----------
-    // Partial sums go out with device-coherent stores; after they complete
-    // (vmcnt 0) the block counts itself in, and the last block of the tile
-    // reads every split's partials with device-coherent loads and adds them
-    // in split order.  No cache-wide write-back or invalidate is needed.
+    // Each wave's partial sums go out as 16-byte device-coherent stores (sc1:
+    // written through to memory, past the XCD-private L2) in a wave-contiguous
+    // layout, [split][tile][wave][piece][lane], so every store instruction
+    // writes 1 KB of consecutive bytes.  After they complete (vmcnt 0) the
+    // block counts itself in; the last block of the tile reads each split's
+    // pieces with device-coherent loads, all pieces of a split in flight at
+    // once, and adds the splits in order 0, 1, 2, ...  No cache-wide
+    // write-back or invalidate is needed.
     if (SPLIT && p.splits > 1) {
-        const size_t plane = (size_t)N * M;
-        float *mine = p.partial + (size_t)split * NW * plane;
+        constexpr int PIECES = NW * TM * TN * 4; // 4 accumulators (16 bytes) per piece
+        const __amdgpu_buffer_rsrc_t prs = make_rsrc(p.partial);
+        const uint32_t lane_off = lane * 16;
+        auto wave_base = [&](int sp) __attribute__((always_inline)) {
+            return (uint32_t)(((sp * ntiles + tile) * NWAVES + wave) * PIECES) * 1024u;
+        };
+        {
+            const uint32_t base = wave_base(split);
 #pragma unroll
-        for (int w = 0; w < NW; ++w)
+            for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int mi = 0; mi < TM; ++mi)
+                for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < TN; ++ni)
+                    for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-                        if (t < N && f < M) {
-                            float *dst = mine + w * plane + (size_t)t * M + f;
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                __hip_atomic_store(dst + e, acc[w][mi][ni][4 * j + e], __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT);
+                        for (int j = 0; j < 4; ++j) {
+                            const int g = ((w * TM + mi) * TN + ni) * 4 + j;
+                            const f32x4 v = {acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
+                                             acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, lane_off,
+                                                                   base + g * 1024u, kCoherent);
                         }
-                    }
+        }
         wait_vmcnt<0>();
         __syncthreads();
         if (tid == 0) {
@@ -411,6 +424,32 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
             return;
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        f32x4 sum[PIECES];
+        for (int sp = 0; sp < p.splits; ++sp) {
+            f32x4 x[PIECES];
+            if (sp == split) {
+#pragma unroll
+                for (int w = 0; w < NW; ++w)
+#pragma unroll
+                    for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                        for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                x[((w * TM + mi) * TN + ni) * 4 + j] =
+                                    f32x4{acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
+                                          acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
+            } else {
+                const uint32_t base = wave_base(sp);
+#pragma unroll
+                for (int g = 0; g < PIECES; ++g)
+                    x[g] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, lane_off, base + g * 1024u, kCoherent));
+            }
+#pragma unroll
+            for (int g = 0; g < PIECES; ++g)
+                sum[g] = sp == 0 ? x[g] : sum[g] + x[g];
+        }
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
@@ -418,25 +457,10 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
 #pragma unroll
                 for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-                        if (t < N && f < M) {
+                    for (int j = 0; j < 4; ++j)
 #pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                float sum = 0.0f;
-                                for (int s = 0; s < p.splits; ++s) {
-                                    const float v =
-                                        s == split ? acc[w][mi][ni][4 * j + e]
-                                                   : __hip_atomic_load(p.partial + ((size_t)s * NW + w) * plane +
-                                                                           (size_t)t * M + f + e,
-                                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                                    sum = s == 0 ? v : sum + v;
-                                }
-                                acc[w][mi][ni][4 * j + e] = sum;
-                            }
-                        }
-                    }
+                        for (int e = 0; e < 4; ++e)
+                            acc[w][mi][ni][4 * j + e] = sum[((w * TM + mi) * TN + ni) * 4 + j][e];
     }
 
     // ---- epilogue: fp32 -> (silu(G) * U) -> bf16, 8-byte row-major stores -----

@@ -1,26 +1,27 @@
 // Split-K streaming GEMV kernels of the Gated MLP for few tokens (T <= 8).
 //
 // With T <= 8 every weight byte is used for at most 8 multiply-adds, so the
-// matmuls of the Gated MLP (Fig. fig:mlp-example, Section 4.1) are bound by
-// the rate at which the weights stream from HBM.  Each block streams a strip
+// matmuls of the Gated MLP (Fig. fig:mlp-example, Section 4.2) are bound by
+// the rate at which the weights stream from HBM.  A work item streams a strip
 // of up to 256 weight columns over a slice of k rows:
 //
 //   * lane (l % 32) owns 8 adjacent columns (one 16-byte load per row); the
 //     two 32-lane halves of a wave and the 4 waves take rows k = g, g+8, ...
 //     (8 row groups), so a wave reads two 512-byte row segments per load
 //     instruction;
-//   * the activations of the slice are staged once in LDS as fp32;
+//   * the activations of a lane's rows are loaded into registers with its
+//     weights (no LDS staging, so no barrier stalls the first loads);
 //   * partial sums are reduced in a fixed order: across the two halves of
 //     the wave by a lane shuffle, across the 4 waves through LDS, and across
-//     the split-K blocks of a strip by the last block to finish (arrival
-//     counter), which adds the per-block sums in split order;
+//     the split-K items of a strip by the last block to finish (arrival
+//     counter), which adds the per-item sums in split order;
 //   * each lane keeps two batches of 16-byte weight loads in flight (the
 //     next batch is issued before the current one is consumed).
 //   The result is therefore bitwise reproducible run to run.
 //
-// The gate/up instantiation (NW = 2) streams Wg and Wu together and its last
-// block applies H = bf16(silu(G) * U); the down instantiation (NW = 1)
-// streams Wd and writes Y = bf16(H Wd).
+// The gate/up kernel (NW = 2) streams Wg and Wu together and its last block
+// applies H = bf16(silu(G) * U); the down kernel (NW = 1) streams Wd and writes
+// Y = bf16(H Wd).
 #pragma once
 
 #include "common.hpp"
@@ -32,7 +33,7 @@ struct GemvParams {
     const uint16_t *w1;  // [K, M] bf16 (Wu) for the gate/up kernel
     const uint16_t *act; // [NT, K] bf16 (X, or H)
     uint16_t *out;       // [NT, M] bf16 (H, or Y)
-    float *partial;      // [splits][NW][NT][M] fp32 per-block sums
+    float *partial;      // [splits][NW][NT][M] fp32 per-item sums
     uint32_t *counters;  // arrival counter per strip (zero on entry and exit)
     int M, K;
     int k_split;     // rows per split, <= gemv_max_split_rows<NT>()
@@ -49,23 +50,26 @@ constexpr int kGemvThreads = 256;
 template <int NT, int NW>
 constexpr int gemv_batch_rows() { return NT <= 2 ? (NW == 1 ? 16 : 8) : 4; }
 
-// Rows of one split: the split's activations are staged in LDS as fp32
-// (NT x rows floats, at most 16 KB).
+// Most rows of one split (bounds the work of one block).
 template <int NT>
 constexpr int gemv_max_split_rows() { return NT <= 2 ? 2048 : 4096 / NT; }
 
+// LDS of one block: per-wave column sums, last-block flag.
+template <int NT, int NW>
+struct GemvShared {
+    float red[4][NW][NT][kGemvMaxStrip];
+    int last;
+};
+
+// One work item (strip, split) of a GEMV step, run by the whole block.
 template <int NT, int NW, int EPI>
-__global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
+__device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh)
 {
     constexpr int RG = 8; // row groups per block
     constexpr int U = gemv_batch_rows<NT, NW>();
-    __shared__ float xs[NT][gemv_max_split_rows<NT>()];
-    __shared__ float red[4][NW][NT][kGemvMaxStrip];
-    __shared__ int s_last;
-
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int strip = blockIdx.x % p.strips;
-    const int split = blockIdx.x / p.strips;
+    const int strip = item % p.strips;
+    const int split = item / p.strips;
     const int M = p.M, K = p.K;
     const int width = 8 * p.strip_lanes;
     const int m0 = strip * width;
@@ -74,38 +78,64 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
 
     const int col = (lane & 31) * 8;
     const int rg = wave * 2 + (lane >> 5);
-    const bool valid = (lane & 31) < p.strip_lanes && m0 + col < M;
 
-    // Weight rows of batch b: rg + 8*(b*U + u), u < U; every lane of the
-    // block runs the same nb batches, the last of which may be partial
-    // (rows past the split are neither loaded nor accumulated).  The loads
-    // bypass caching (each weight byte is read once).
+    // Batch b covers rows [8*U*b, 8*U*(b+1)) of the split; row group rg takes
+    // the U consecutive rows from (8*b + rg)*U.  Every lane of the block runs
+    // the same nb batches, the last of which may be partial.  A batch is one
+    // load of the U activations of each token (issued first) and U weight
+    // loads per weight, all unconditional, so the compiler counts them and
+    // waits for exactly the batch it consumes: a lane past the strip's last
+    // column reloads that column, and a row past the split reloads a row of
+    // the split (neither is accumulated into a stored result).  The weight
+    // loads bypass caching (each weight byte is read once).
+    const int lcol = min(m0 + col, M - 8);
     const uint16_t *wp[NW];
-    wp[0] = p.w0 + (size_t)kb * M + m0 + col;
+    wp[0] = p.w0 + (size_t)kb * M + lcol;
     if constexpr (NW == 2)
-        wp[1] = p.w1 + (size_t)kb * M + m0 + col;
-    auto load_batch = [&](u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
+        wp[1] = p.w1 + (size_t)kb * M + lcol;
+    const uint16_t *xp = p.act + kb;
+    constexpr int XW = U / 2; // activation words (2 bf16 each) per token per batch
+    struct Batch {
+        uint32_t x[NT][XW];
+        u32x4 w[U][NW];
+    };
+    auto load_batch = [&](Batch &v, int b) __attribute__((always_inline)) {
+        const int r0 = (8 * b + rg) * U;
+        // Activation pieces of 8 (U >= 8) or 4 (U = 4) rows lie wholly in
+        // or out of the split (nrows and r0 are multiples of 8, resp. 4).
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            if constexpr (U >= 8) {
+#pragma unroll
+                for (int q = 0; q < U / 8; ++q) {
+                    const int r = r0 + 8 * q < nrows ? r0 + 8 * q : 0;
+                    const u32x4 x4 = *(const u32x4 *)(xp + (size_t)t * K + r);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v.x[t][4 * q + e] = x4[e];
+                }
+            } else {
+                const int r = r0 < nrows ? r0 : 0;
+                const u32x2 x2 = *(const u32x2 *)(xp + (size_t)t * K + r);
+                v.x[t][0] = x2[0];
+                v.x[t][1] = x2[1];
+            }
+        }
+        // The activations must be issued before the weights: loads complete
+        // in order, so waiting for a batch's weights then covers them too.
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int r = rg + RG * (b * U + u);
+            const int r = min(r0 + u, nrows - 1);
 #pragma unroll
             for (int w = 0; w < NW; ++w)
-                v[u][w] = r < nrows ? __builtin_nontemporal_load((const u32x4 *)(wp[w] + (size_t)r * M))
-                                    : u32x4{0u, 0u, 0u, 0u};
+                v.w[u][w] = __builtin_nontemporal_load((const u32x4 *)(wp[w] + (size_t)r * M));
         }
     };
     const int nb = (nrows + RG * U - 1) / (RG * U);
-    u32x4 va[U][NW], vb[U][NW];
-    // The first weight batch is in flight while the activations are staged.
-    if (valid && nb > 0)
-        load_batch(va, 0);
-
-    // Stage this slice of the activations as fp32.
-    for (int i = tid; i < NT * nrows; i += kGemvThreads) {
-        const int t = i / nrows, r = i - t * nrows;
-        xs[t][r] = __builtin_bit_cast(float, (uint32_t)p.act[(size_t)t * K + kb + r] << 16);
-    }
-    __syncthreads();
+    Batch va, vb;
+    load_batch(va, 0);
+    load_batch(vb, 1); // past the split if nb == 1 (never accumulated)
 
     float acc[NW][NT][8];
 #pragma unroll
@@ -116,37 +146,42 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
             for (int e = 0; e < 8; ++e)
                 acc[w][t][e] = 0.0f;
 
-    if (valid) {
-        auto fma_row = [&](const u32x4 (&v)[NW], int r) __attribute__((always_inline)) {
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const float x = xs[t][r];
-#pragma unroll
-                for (int w = 0; w < NW; ++w)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc[w][t][2 * e] += x * bf16_lo(v[w][e]);
-                        acc[w][t][2 * e + 1] += x * bf16_hi(v[w][e]);
-                    }
-            }
-        };
-        auto fma_batch = [&](const u32x4 (&v)[U][NW], int b) __attribute__((always_inline)) {
+    {
+        auto fma_batch = [&](const Batch &v, int b) __attribute__((always_inline)) {
+            const int r0 = (8 * b + rg) * U;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int r = rg + RG * (b * U + u);
-                if (r < nrows)
-                    fma_row(v[u], r);
+                if (r0 + u < nrows) {
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        const float x = u & 1 ? bf16_hi(v.x[t][u / 2]) : bf16_lo(v.x[t][u / 2]);
+#pragma unroll
+                        for (int w = 0; w < NW; ++w)
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                acc[w][t][2 * e] += x * bf16_lo(v.w[u][w][e]);
+                                acc[w][t][2 * e + 1] += x * bf16_hi(v.w[u][w][e]);
+                            }
+                    }
+                }
             }
         };
-        for (int b = 0; b < nb; b += 2) {
-            if (b + 1 < nb)
-                load_batch(vb, b + 1);
+        // Steady state: two batches in flight, loads unconditional.
+        int b = 0;
+        for (; b + 3 < nb; b += 2) {
             fma_batch(va, b);
-            if (b + 2 < nb)
-                load_batch(va, b + 2);
-            if (b + 1 < nb)
-                fma_batch(vb, b + 1);
+            load_batch(va, b + 2);
+            fma_batch(vb, b + 1);
+            load_batch(vb, b + 3);
         }
+        // The last one to three batches.
+        fma_batch(va, b);
+        if (b + 2 < nb)
+            load_batch(va, b + 2);
+        if (b + 1 < nb)
+            fma_batch(vb, b + 1);
+        if (b + 2 < nb)
+            fma_batch(va, b + 2);
     }
 
     // Row groups 2*wave and 2*wave+1 share columns: add the two wave halves.
@@ -164,8 +199,8 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
             for (int t = 0; t < NT; ++t) {
                 f32x4 lo = {acc[w][t][0], acc[w][t][1], acc[w][t][2], acc[w][t][3]};
                 f32x4 hi = {acc[w][t][4], acc[w][t][5], acc[w][t][6], acc[w][t][7]};
-                *(f32x4 *)&red[wave][w][t][col] = lo;
-                *(f32x4 *)&red[wave][w][t][col + 4] = hi;
+                *(f32x4 *)&sh.red[wave][w][t][col] = lo;
+                *(f32x4 *)&sh.red[wave][w][t][col + 4] = hi;
             }
     }
     __syncthreads();
@@ -178,10 +213,11 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
     for (int w = 0; w < NW; ++w)
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            v[w][t] = ((red[0][w][t][tid] + red[1][w][t][tid]) + red[2][w][t][tid]) + red[3][w][t][tid];
+            v[w][t] = ((sh.red[0][w][t][tid] + sh.red[1][w][t][tid]) + sh.red[2][w][t][tid]) +
+                      sh.red[3][w][t][tid];
 
     if (p.splits > 1) {
-        // Per-block sums go out with device-coherent stores; once they have
+        // Per-item sums go out with device-coherent stores; once they have
         // completed (vmcnt 0) the block counts itself in.  The block that
         // arrives last reads every split's sums with device-coherent loads.
         // No cache-wide write-back or invalidate is needed.
@@ -198,43 +234,49 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
         if (tid == 0) {
             const uint32_t before =
                 __hip_atomic_fetch_add(p.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_last = before == (uint32_t)(p.splits - 1);
+            sh.last = before == (uint32_t)(p.splits - 1);
         }
         __syncthreads();
-        if (!s_last)
+        if (!sh.last)
             return;
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (mvalid) {
-            // Sum the splits in order 0, 1, 2, ...; loads are issued eight
-            // at a time so their latencies overlap.
-            constexpr int B = 8;
+            // Sum the splits in order 0, 1, 2, ...; the loads of C splits
+            // (about 32 values per thread) are in flight at once.
+            constexpr int C = NW * NT >= 32 ? 1 : 32 / (NW * NT);
+            const size_t stride = (size_t)NW * NT * M;
+            const float *src = &p.partial[m];
+            float sum[NW][NT];
+            for (int s0 = 0; s0 < p.splits; s0 += C) {
+                float x[C][NW][NT];
+#pragma unroll
+                for (int u = 0; u < C; ++u)
+#pragma unroll
+                    for (int w = 0; w < NW; ++w)
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+                            const int sp = s0 + u;
+                            x[u][w][t] = sp == split ? v[w][t]
+                                         : sp < p.splits
+                                             ? __hip_atomic_load(src + sp * stride + ((size_t)w * NT + t) * M,
+                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                             : 0.0f;
+                        }
+#pragma unroll
+                for (int u = 0; u < C; ++u)
+                    if (s0 + u < p.splits)
+#pragma unroll
+                        for (int w = 0; w < NW; ++w)
+#pragma unroll
+                            for (int t = 0; t < NT; ++t)
+                                sum[w][t] = s0 + u == 0 ? x[u][w][t] : sum[w][t] + x[u][w][t];
+            }
 #pragma unroll
             for (int w = 0; w < NW; ++w)
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const float own = v[w][t];
-                    const float *src = &p.partial[((size_t)w * NT + t) * M + m];
-                    const size_t stride = (size_t)NW * NT * M;
-                    float s = 0.0f;
-                    for (int s0 = 0; s0 < p.splits; s0 += B) {
-                        float x[B];
-#pragma unroll
-                        for (int u = 0; u < B; ++u) {
-                            const int sp = s0 + u;
-                            x[u] = sp == split ? own
-                                   : sp < p.splits
-                                       ? __hip_atomic_load(src + sp * stride, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT)
-                                       : 0.0f;
-                        }
-#pragma unroll
-                        for (int u = 0; u < B; ++u)
-                            if (s0 + u < p.splits)
-                                s = s0 + u == 0 ? x[u] : s + x[u];
-                    }
-                    v[w][t] = s;
-                }
+                for (int t = 0; t < NT; ++t)
+                    v[w][t] = sum[w][t];
         }
     }
 
@@ -249,6 +291,13 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
             p.out[(size_t)t * M + m] = __builtin_bit_cast(uint16_t, (__bf16)y);
         }
     }
+}
+
+template <int NT, int NW, int EPI>
+__global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
+{
+    __shared__ GemvShared<NT, NW> sh;
+    gemv_item<NT, NW, EPI>(p, blockIdx.x, sh);
 }
 
 } // namespace gmlp

@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <string>
 
 #include "gmlp.h"
 #include "gemm_mfma.hpp"
@@ -82,6 +83,7 @@ struct Plan {
     Step gate_up, down;
 };
 
+
 struct Layout {
     size_t counters_off = 0, h_off = 0, partial_off = 0, total = 0;
     int counters = 0; // most arrival counters any path uses for this shape
@@ -120,7 +122,8 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.blocks = tiles * s.splits;
     s.threads = S::NTHREADS;
     s.counters = s.splits > 1 ? tiles : 0;
-    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
+    // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane].
+    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * tiles * S::BMW * S::BN * nw * sizeof(float) : 0;
 }
 
 template <int NT>
@@ -309,13 +312,15 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.group_m = s.group_m;
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
+    if (s.partial_bytes > (size_t)kNumRecords)
+        return fail(GMLP_ERR_UNSUPPORTED, "split-K partial sums of %zu bytes exceed the 2 GiB buffer range",
+                    s.partial_bytes);
     hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
     return hip_check(hipGetLastError(), "MFMA GEMM launch");
 }
 
-template <int NT, int NW, int EPI>
-int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                   uint8_t *ws, const Layout &l, hipStream_t stream)
+GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                       uint8_t *ws, const Layout &l)
 {
     GemvParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -330,6 +335,14 @@ int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *ac
     p.splits = s.splits;
     p.strips = s.strips;
     p.strip_lanes = s.strip_lanes;
+    return p;
+}
+
+template <int NT, int NW, int EPI>
+int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                   uint8_t *ws, const Layout &l, hipStream_t stream)
+{
+    const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l);
     hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI>), dim3(s.blocks), dim3(kGemvThreads), 0,
                        stream, p);
     return hip_check(hipGetLastError(), "GEMV launch");
@@ -351,6 +364,7 @@ int launch_gemv(const Step &s, const void *w0, const void *w1, const void *act, 
     default: return fail(GMLP_ERR_INVALID_ARG, "GEMV path needs 1 <= T <= 8 (T=%d)", s.N);
     }
 }
+
 
 int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, void *H, uint8_t *ws,
                 const Layout &l, hipStream_t st)
@@ -419,6 +433,28 @@ struct Scratch {
     }
 };
 
+template <class S>
+std::string shape_name()
+{
+    return "GemmShape<" + std::to_string(S::NW) + ", " + std::to_string(S::WM) + ", " +
+           std::to_string(S::WN) + ", " + std::to_string(S::TM) + ", " + std::to_string(S::TN) + ", " +
+           std::to_string(S::STAGES) + ", " + std::to_string(S::BK) + ">";
+}
+
+// A step's kernel as a profiler names it, without the namespace.
+std::string kernel_name(const Step &s, bool gate_up)
+{
+    switch (s.kind) {
+    case K_GEMM_GU_L: return "gemm_mfma_kernel<" + shape_name<GateUpLarge>() + ", 0, false>";
+    case K_GEMM_GU_S: return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true>";
+    case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false>";
+    case K_GEMM_DN_S: return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true>";
+    case K_GEMV:
+        return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0>" : ", 1, 1>");
+    default: return "none";
+    }
+}
+
 } // namespace
 
 extern "C" {
@@ -444,6 +480,31 @@ int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg
 {
     int rc = validate(T, D, F, X, Wg, Wu, Wd, Y);
     return rc ? rc : ok();
+}
+
+int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t bytes)
+{
+    int rc;
+    if (!buf || !bytes)
+        return fail(GMLP_ERR_INVALID_ARG, "describe needs a buffer");
+    buf[0] = '\0';
+    if ((rc = check_shape(T, D, F)) || (rc = check_path(path, T)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Plan plan = make_plan(T, D, F, path);
+    std::string text;
+    auto line = [&](const char *name, int blocks, int threads, int splits) {
+        char tmp[160];
+        snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", name, blocks, threads, splits);
+        text += tmp;
+    };
+    for (const Step *s : {&plan.gate_up, &plan.down}) {
+        const std::string name = kernel_name(*s, s == &plan.gate_up);
+        line(name.c_str(), s->blocks, s->threads, s->splits);
+    }
+    snprintf(buf, bytes, "%s", text.c_str());
+    return ok();
 }
 
 size_t gmlp_workspace_size(int64_t T, int64_t D, int64_t F)

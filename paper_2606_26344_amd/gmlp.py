@@ -37,6 +37,7 @@ _SIGNATURES = {
     "gmlp_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "gmlp_last_error": ([], ctypes.c_char_p),
     "gmlp_validate": ([_I64, _I64, _I64, _P, _P, _P, _P, _P], ctypes.c_int),
+    "gmlp_describe": ([_I64, _I64, _I64, ctypes.c_int, ctypes.c_char_p, _SZ], ctypes.c_int),
     "gmlp_workspace_size": ([_I64, _I64, _I64], _SZ),
     "gmlp_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
     "gmlp_forward": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
@@ -119,6 +120,19 @@ def _expect(t: torch.Tensor, name: str, shape, device) -> None:
         raise ValueError("%s must be contiguous" % name)
     if tuple(t.shape) != tuple(shape):
         raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+
+
+def describe(T: int, D: int, F: int, path: str = "auto") -> list:
+    """The kernels forward() enqueues for this shape: a list of
+    (name, grid, block, k_splits), in launch order."""
+    buf = ctypes.create_string_buffer(1024)
+    _check(library().gmlp_describe(T, D, F, _PATHS[path], buf, len(buf)))
+    out = []
+    for line in buf.value.decode().splitlines():
+        name, rest = line.rsplit(" grid=", 1)
+        grid, block, splits = (int(f.split("=")[1]) for f in ("grid=" + rest).split())
+        out.append((name, grid, block, splits))
+    return out
 
 
 def workspace_size(T: int, D: int, F: int) -> int:

@@ -96,3 +96,23 @@ def test_helpers_validate_too(lib):
     assert lib.gmlp_gate_up(A, A + 64 * MB, A + 128 * MB, A, 4, 256, 512, None) == 1  # H on X
     assert lib.gmlp_down(A, A + 64 * MB, None, 4, 512, 256, None) == 1
     assert lib.gmlp_down(A, A + 64 * MB, A + 8, 4, 512, 256, None) == 2
+
+
+def test_describe_names_the_kernels_of_each_path(lib):
+    gemv = gmlp.describe(1, 4096, 14336)
+    assert [k[0] for k in gemv] == ["gemv_splitk_kernel<1, 2, 0>", "gemv_splitk_kernel<1, 1, 1>"]
+    for name, grid, block, splits in gemv:
+        assert block == 256 and grid >= 256 and splits > 1
+    big = gmlp.describe(4096, 4096, 14336)
+    assert [k[0].split("<")[0] for k in big] == ["gemm_mfma_kernel", "gemm_mfma_kernel"]
+    assert big[0][0].endswith(", 0, false>") and big[1][0].endswith(", 1, false>")
+    assert gmlp.describe(0, 256, 512) == []
+
+
+def test_describe_rejects_bad_arguments(lib):
+    buf = ctypes.create_string_buffer(64)
+    assert lib.gmlp_describe(4, 260, 512, 0, buf, 64) == 2
+    assert lib.gmlp_describe(9, 256, 512, 1, buf, 64) == 2  # GEMV needs T <= 8
+    assert lib.gmlp_describe(4, 256, 512, 3, buf, 64) == 1  # unknown path
+    assert lib.gmlp_describe(4, 256, 512, 0, None, 64) == 1
+    assert lib.gmlp_describe(4, 256, 512, 0, buf, 8) == 0 and len(buf.value) == 7  # truncated
