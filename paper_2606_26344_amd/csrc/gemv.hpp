@@ -15,8 +15,8 @@
 //     the wave by a lane shuffle, across the 4 waves through LDS, and across
 //     the split-K items of a strip by the last block to finish (arrival
 //     counter), which adds the per-item sums in split order;
-//   * each lane keeps two batches of 16-byte weight loads in flight (the
-//     next batch is issued before the current one is consumed).
+//   * each lane keeps two or three batches of 16-byte weight loads in
+//     flight (a batch is reissued as soon as it has been consumed).
 //   The result is therefore bitwise reproducible run to run.
 //
 // The gate/up kernel (NW = 2) streams Wg and Wu together and its last block
@@ -45,10 +45,13 @@ struct GemvParams {
 constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
 constexpr int kGemvThreads = 256;
 
-// Weight rows per lane per load batch: 2*NW*U loads of 16 bytes in flight
-// per lane (two batches), within the register budget of NT tokens.
-template <int NT, int NW>
-constexpr int gemv_batch_rows() { return NT <= 2 ? (NW == 1 ? 16 : 8) : 4; }
+// Weight rows per lane per load batch (U), and batches in flight per lane
+// (DEPTH): DEPTH*NW*U loads of 16 bytes in flight per lane, within the
+// register budget of NT tokens.
+template <int NT>
+constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : NT <= 6 ? 4 : 2; }
+template <int NT>
+constexpr int gemv_depth() { return 2; }
 
 // Most rows of one split (bounds the work of one block).
 template <int NT>
@@ -66,7 +69,7 @@ template <int NT, int NW, int EPI>
 __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh)
 {
     constexpr int RG = 8; // row groups per block
-    constexpr int U = gemv_batch_rows<NT, NW>();
+    constexpr int U = gemv_batch_rows<NT>();
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int strip = item % p.strips;
     const int split = item / p.strips;
@@ -101,8 +104,8 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
     };
     auto load_batch = [&](Batch &v, int b) __attribute__((always_inline)) {
         const int r0 = (8 * b + rg) * U;
-        // Activation pieces of 8 (U >= 8) or 4 (U = 4) rows lie wholly in
-        // or out of the split (nrows and r0 are multiples of 8, resp. 4).
+        // Activation pieces of min(U, 8) rows lie wholly in or out of the
+        // split (nrows is a multiple of 8, r0 of U).
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (U >= 8) {
@@ -114,11 +117,14 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                     for (int e = 0; e < 4; ++e)
                         v.x[t][4 * q + e] = x4[e];
                 }
-            } else {
+            } else if constexpr (U == 4) {
                 const int r = r0 < nrows ? r0 : 0;
                 const u32x2 x2 = *(const u32x2 *)(xp + (size_t)t * K + r);
                 v.x[t][0] = x2[0];
                 v.x[t][1] = x2[1];
+            } else {
+                const int r = r0 < nrows ? r0 : 0;
+                v.x[t][0] = *(const uint32_t *)(xp + (size_t)t * K + r);
             }
         }
         // The activations must be issued before the weights: loads complete
@@ -132,10 +138,12 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                 v.w[u][w] = __builtin_nontemporal_load((const u32x4 *)(wp[w] + (size_t)r * M));
         }
     };
+    constexpr int DEPTH = gemv_depth<NT>();
     const int nb = (nrows + RG * U - 1) / (RG * U);
-    Batch va, vb;
-    load_batch(va, 0);
-    load_batch(vb, 1); // past the split if nb == 1 (never accumulated)
+    Batch ring[DEPTH];
+#pragma unroll
+    for (int i = 0; i < DEPTH; ++i)
+        load_batch(ring[i], i); // past the split if i >= nb (never accumulated)
 
     float acc[NW][NT][8];
 #pragma unroll
@@ -147,41 +155,47 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                 acc[w][t][e] = 0.0f;
 
     {
-        auto fma_batch = [&](const Batch &v, int b) __attribute__((always_inline)) {
+        auto fma_batch = [&](const Batch &bt, int b) __attribute__((always_inline)) {
             const int r0 = (8 * b + rg) * U;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (r0 + u < nrows) {
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
-                        const float x = u & 1 ? bf16_hi(v.x[t][u / 2]) : bf16_lo(v.x[t][u / 2]);
+                        const float x = u & 1 ? bf16_hi(bt.x[t][u / 2]) : bf16_lo(bt.x[t][u / 2]);
 #pragma unroll
                         for (int w = 0; w < NW; ++w)
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
-                                acc[w][t][2 * e] += x * bf16_lo(v.w[u][w][e]);
-                                acc[w][t][2 * e + 1] += x * bf16_hi(v.w[u][w][e]);
+                                acc[w][t][2 * e] += x * bf16_lo(bt.w[u][w][e]);
+                                acc[w][t][2 * e + 1] += x * bf16_hi(bt.w[u][w][e]);
                             }
                     }
                 }
             }
         };
-        // Steady state: two batches in flight, loads unconditional.
+        // Steady state: DEPTH batches in flight, loads unconditional.  Batch
+        // b lives in ring[b % DEPTH].
         int b = 0;
-        for (; b + 3 < nb; b += 2) {
-            fma_batch(va, b);
-            load_batch(va, b + 2);
-            fma_batch(vb, b + 1);
-            load_batch(vb, b + 3);
+        for (; b + 2 * DEPTH - 1 < nb; b += DEPTH) {
+#pragma unroll
+            for (int i = 0; i < DEPTH; ++i) {
+                fma_batch(ring[i], b + i);
+                load_batch(ring[i], b + i + DEPTH);
+            }
         }
-        // The last one to three batches.
-        fma_batch(va, b);
-        if (b + 2 < nb)
-            load_batch(va, b + 2);
-        if (b + 1 < nb)
-            fma_batch(vb, b + 1);
-        if (b + 2 < nb)
-            fma_batch(va, b + 2);
+        // The last 1 .. 2*DEPTH-1 batches.
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i) {
+            if (b + i < nb)
+                fma_batch(ring[i], b + i);
+            if (b + i + DEPTH < nb)
+                load_batch(ring[i], b + i + DEPTH);
+        }
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i)
+            if (b + i + DEPTH < nb)
+                fma_batch(ring[i], b + i + DEPTH);
     }
 
     // Row groups 2*wave and 2*wave+1 share columns: add the two wave halves.
@@ -293,8 +307,10 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
     }
 }
 
+// At most 256 VGPRs per lane: two blocks per CU stay resident.
 template <int NT, int NW, int EPI>
-__global__ __launch_bounds__(kGemvThreads) void gemv_splitk_kernel(GemvParams p)
+__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void gemv_splitk_kernel(GemvParams p)
 {
     __shared__ GemvShared<NT, NW> sh;
     gemv_item<NT, NW, EPI>(p, blockIdx.x, sh);

@@ -41,7 +41,7 @@ int ok()
 // ---- tile configurations -------------------------------------------------
 //                          NW WM WN TM TN STAGES BK
 using GateUpLarge = GemmShape<2, 2, 2, 2, 4, 3, 32>; // 128 F cols x 256 tokens, per weight
-using GateUpSmall = GemmShape<2, 2, 2, 1, 2, 4, 64>; //  64 F cols x 128 tokens
+using GateUpSmall = GemmShape<2, 4, 2, 1, 2, 3, 64>; // 128 F cols x 128 tokens, 8 waves
 using DownLarge = GemmShape<1, 2, 2, 4, 4, 4, 32>;   // 256 D cols x 256 tokens
 using DownSmall = GemmShape<1, 2, 2, 2, 2, 4, 64>;   // 128 D cols x 128 tokens
 // Column tiles swept per token tile by consecutive blocks (L2 locality),
@@ -89,14 +89,17 @@ struct Layout {
     int counters = 0; // most arrival counters any path uses for this shape
 };
 
-// Split K so that about `target` blocks run, keeping at least `min_tiles`
-// k-tiles of `tile_k` rows per split.
+// Split K so that at most `target` blocks run (the small-T kernels hold one
+// block per CU: a second round of blocks would cost a whole tile's time),
+// keeping at least `min_tiles` k-tiles of `tile_k` rows per split.  Each
+// split adds T x columns fp32 partial sums to write and read back, so the
+// count rounds down.
 void choose_splits(Step &s, int tiles, int target, int tile_k, int min_tiles)
 {
     const int64_t ktiles = cdiv(s.K, tile_k);
     int64_t splits = 1;
     if (tiles < target)
-        splits = std::min<int64_t>(cdiv(target, tiles), std::max<int64_t>(1, ktiles / min_tiles));
+        splits = std::min<int64_t>(target / tiles, std::max<int64_t>(1, ktiles / min_tiles));
     const int64_t per = cdiv(ktiles, splits);
     s.k_split = (int)(per * tile_k);
     s.splits = (int)cdiv(s.K, s.k_split);
@@ -126,31 +129,34 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.partial_bytes = s.splits > 1 ? (size_t)s.splits * tiles * S::BMW * S::BN * nw * sizeof(float) : 0;
 }
 
-template <int NT>
-constexpr int gemv_rows_limit()
-{
-    return gemv_max_split_rows<NT>();
-}
-
+// Per token count: most rows of a split, and rows per load batch of the 8
+// row groups (splits are whole batches).
 int gemv_max_rows(int nt)
 {
     switch (nt) {
-    case 1: return gemv_rows_limit<1>();
-    case 2: return gemv_rows_limit<2>();
-    case 3: return gemv_rows_limit<3>();
-    case 4: return gemv_rows_limit<4>();
-    case 5: return gemv_rows_limit<5>();
-    case 6: return gemv_rows_limit<6>();
-    case 7: return gemv_rows_limit<7>();
-    default: return gemv_rows_limit<8>();
+    case 1: return gemv_max_split_rows<1>();
+    case 2: return gemv_max_split_rows<2>();
+    case 3: return gemv_max_split_rows<3>();
+    case 4: return gemv_max_split_rows<4>();
+    case 5: return gemv_max_split_rows<5>();
+    case 6: return gemv_max_split_rows<6>();
+    case 7: return gemv_max_split_rows<7>();
+    default: return gemv_max_split_rows<8>();
     }
 }
 
-// Rows one GEMV lane streams per load batch, times the 8 row groups.
-int gemv_batch_span(int nt, int nw)
+int gemv_batch_span(int nt)
 {
-    return 8 * (nt <= 2 ? (nw == 1 ? gemv_batch_rows<1, 1>() : gemv_batch_rows<1, 2>())
-                        : gemv_batch_rows<8, 2>());
+    switch (nt) {
+    case 1: return 8 * gemv_batch_rows<1>();
+    case 2: return 8 * gemv_batch_rows<2>();
+    case 3: return 8 * gemv_batch_rows<3>();
+    case 4: return 8 * gemv_batch_rows<4>();
+    case 5: return 8 * gemv_batch_rows<5>();
+    case 6: return 8 * gemv_batch_rows<6>();
+    case 7: return 8 * gemv_batch_rows<7>();
+    default: return 8 * gemv_batch_rows<8>();
+    }
 }
 
 // GEMV decomposition: strips of 256 columns (32 lanes x 8) times k splits.
@@ -169,7 +175,7 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.strip_lanes = 32;
     s.strips = (int)cdiv(M, 8 * s.strip_lanes);
     const int max_rows = gemv_max_rows(N);
-    const int span = gemv_batch_span(N, nw);
+    const int span = gemv_batch_span(N);
     const int64_t lo = std::max<int64_t>(cdiv(K, max_rows), cdiv(384, s.strips));
     const int64_t hi = std::max<int64_t>(lo, cdiv(K, span));
     int64_t rows = 0;
