@@ -36,7 +36,7 @@ struct GemvParams {
     float *partial;      // [splits][NW][NT][M] fp32 per-item sums
     uint32_t *counters;  // arrival counter per strip (zero on entry and exit)
     int M, K;
-    int k_split;     // rows per split, <= gemv_max_split_rows<NT>()
+    int k_split;     // rows per split (a multiple of the load batch span)
     int splits;
     int strips;
     int strip_lanes; // lanes per row (8 columns each, <= 32): strip width 8 * strip_lanes
@@ -53,9 +53,6 @@ constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : NT <= 6 ? 4 : 2; }
 template <int NT>
 constexpr int gemv_depth() { return 2; }
 
-// Most rows of one split (bounds the work of one block).
-template <int NT>
-constexpr int gemv_max_split_rows() { return NT <= 2 ? 2048 : 4096 / NT; }
 
 // LDS of one block: per-wave column sums, last-block flag.
 template <int NT, int NW>

@@ -129,22 +129,8 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.partial_bytes = s.splits > 1 ? (size_t)s.splits * tiles * S::BMW * S::BN * nw * sizeof(float) : 0;
 }
 
-// Per token count: most rows of a split, and rows per load batch of the 8
-// row groups (splits are whole batches).
-int gemv_max_rows(int nt)
-{
-    switch (nt) {
-    case 1: return gemv_max_split_rows<1>();
-    case 2: return gemv_max_split_rows<2>();
-    case 3: return gemv_max_split_rows<3>();
-    case 4: return gemv_max_split_rows<4>();
-    case 5: return gemv_max_split_rows<5>();
-    case 6: return gemv_max_split_rows<6>();
-    case 7: return gemv_max_split_rows<7>();
-    default: return gemv_max_split_rows<8>();
-    }
-}
-
+// Rows per load batch of the 8 row groups, per token count (splits are
+// whole batches).
 int gemv_batch_span(int nt)
 {
     switch (nt) {
@@ -160,11 +146,14 @@ int gemv_batch_span(int nt)
 }
 
 // GEMV decomposition: strips of 256 columns (32 lanes x 8) times k splits.
-// The kernels are bound by HBM, not by any one CU, so blocks need not be
-// spread evenly over CUs; what matters is enough blocks (and loads) in
-// flight, equal splits of whole load batches, and few splits (each adds a
-// partial sum to the final reduction).  Measured on MI355X at D=4096,
-// F=14336: about 400-500 blocks, splits of whole batches.
+// Measured on MI355X at D=4096, F=14336 (T=1): one block per CU at most, as
+// few splits as that allows, and splits of whole load batches are fastest
+// (gate/up 56 strips x 4 splits, down 16 x 14: 224 blocks of 1024 rows);
+// more, shorter blocks add partial sums and reduction latency, and a second
+// block on a CU does not raise its share of HBM bandwidth.
+// With more tokens the FMA work per weight byte grows: two blocks per CU.
+int gemv_block_target(int nt) { return nt <= 4 ? 256 : 512; }
+
 void gemv_step(Step &s, int M, int N, int K, int nw)
 {
     s.kind = K_GEMV;
@@ -174,18 +163,14 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.threads = kGemvThreads;
     s.strip_lanes = 32;
     s.strips = (int)cdiv(M, 8 * s.strip_lanes);
-    const int max_rows = gemv_max_rows(N);
     const int span = gemv_batch_span(N);
-    const int64_t lo = std::max<int64_t>(cdiv(K, max_rows), cdiv(384, s.strips));
-    const int64_t hi = std::max<int64_t>(lo, cdiv(K, span));
+    const int64_t max_sp = std::max<int64_t>(1, std::min<int64_t>(gemv_block_target(N) / s.strips, cdiv(K, span)));
     int64_t rows = 0;
-    for (int64_t sp = lo; sp <= std::min<int64_t>(hi, 4 * lo) && !rows; ++sp)
-        if (K % sp == 0 && (K / sp) % span == 0 && K / sp <= max_rows)
+    for (int64_t sp = max_sp; sp >= 1 && !rows; --sp)
+        if (K % sp == 0 && (K / sp) % span == 0)
             rows = K / sp; // equal splits of whole batches
-    if (!rows) {
-        const int64_t sp = std::min(lo, hi);
-        rows = std::min<int64_t>(max_rows, cdiv(cdiv(K, sp), span) * span);
-    }
+    if (!rows || K / rows < max_sp / 2)
+        rows = cdiv(cdiv(K, max_sp), span) * span; // nearly equal splits of whole batches
     s.k_split = (int)rows;
     s.splits = (int)cdiv(K, rows);
     s.blocks = s.strips * s.splits;

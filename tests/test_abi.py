@@ -102,7 +102,7 @@ def test_describe_names_the_kernels_of_each_path(lib):
     gemv = gmlp.describe(1, 4096, 14336)
     assert [k[0] for k in gemv] == ["gemv_splitk_kernel<1, 2, 0>", "gemv_splitk_kernel<1, 1, 1>"]
     for name, grid, block, splits in gemv:
-        assert block == 256 and grid >= 256 and splits > 1
+        assert block == 256 and 128 < grid <= 256 and splits > 1
     big = gmlp.describe(4096, 4096, 14336)
     assert [k[0].split("<")[0] for k in big] == ["gemm_mfma_kernel", "gemm_mfma_kernel"]
     assert big[0][0].endswith(", 0, false>") and big[1][0].endswith(", 1, false>")
@@ -116,3 +116,13 @@ def test_describe_rejects_bad_arguments(lib):
     assert lib.gmlp_describe(4, 256, 512, 3, buf, 64) == 1  # unknown path
     assert lib.gmlp_describe(4, 256, 512, 0, None, 64) == 1
     assert lib.gmlp_describe(4, 256, 512, 0, buf, 8) == 0 and len(buf.value) == 7  # truncated
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 5, 8])
+@pytest.mark.parametrize("D,F", [(4096, 14336), (8192, 28672), (264, 520), (4104, 2056), (8, 8)])
+def test_gemv_plan_covers_k_with_at_most_one_round_of_blocks(lib, T, D, F):
+    for (name, grid, block, splits), (M, K) in zip(gmlp.describe(T, D, F, "gemv"), [(F, D), (D, F)]):
+        strips = -(-M // 256)
+        assert grid == strips * splits and block == 256
+        assert splits <= K // 8 + 1
+        assert grid <= max(512, strips)
