@@ -1,9 +1,10 @@
-"""Pure-Python scalar brute force of the SiLU Gated MLP, for tiny shapes.
+"""Pure-Python scalar brute force of the Gated MLP, for tiny shapes.
 
 TEST INFRASTRUCTURE ONLY.  It is a second, independent spelling of the
-definition (Fig. fig:mlp-example, Section 4.1; matmul as a sum of products,
-Fig. fig:op-sema; silu(x) = x * sigmoid(x), table tab:nki-ops) in plain
-Python floats and nested loops, used to pin the C oracle on small inputs.
+definition (Fig. fig:mlp-example, Section 4.2; matmul as a sum of products,
+Fig. fig:op-sema; silu(x) = x * sigmoid(x), table tab:nki-ops; RMSNorm,
+the equation of Section 2) in plain Python floats and nested loops, used to
+pin the C oracle on small inputs.
 """
 from __future__ import annotations
 
@@ -18,19 +19,41 @@ def brute_silu(z: float) -> float:
     return z * (e / (1.0 + e))
 
 
-def brute_gated_mlp(X, Wg, Wu, Wd):
+def brute_sigmoid(z: float) -> float:
+    if z >= 0:
+        return 1.0 / (1.0 + math.exp(-z))
+    e = math.exp(z)
+    return e / (1.0 + e)
+
+
+def brute_gate(g: float, activation: str = "silu", beta: float = 1.0) -> float:
+    if activation == "silu":
+        return brute_silu(g)
+    if activation == "swish":
+        return g * brute_sigmoid(beta * g)
+    if activation == "sigmoid":
+        return brute_sigmoid(g)
+    raise ValueError(activation)
+
+
+def brute_gated_mlp(X, Wg, Wu, Wd, activation="silu", beta=1.0, rmsnorm=False, eps=0.0):
     """X [T][D], Wg [D][F], Wu [D][F], Wd [F][D] as nested lists of floats."""
     T, D, F = len(X), len(Wg), len(Wg[0])
     Y = []
     for t in range(T):
+        x = list(X[t])
+        if rmsnorm:
+            ms = sum(v * v for v in x) / D
+            r = 1.0 / math.sqrt(ms + eps)
+            x = [v * r for v in x]
         H = []
         for f in range(F):
             g = 0.0
             u = 0.0
             for d in range(D):
-                g += X[t][d] * Wg[d][f]
-                u += X[t][d] * Wu[d][f]
-            H.append(brute_silu(g) * u)
+                g += x[d] * Wg[d][f]
+                u += x[d] * Wu[d][f]
+            H.append(brute_gate(g, activation, beta) * u)
         row = []
         for j in range(D):
             acc = 0.0

@@ -1,5 +1,6 @@
 /*
- * CPU fp64 oracle for the SiLU Gated MLP  Y = (silu(X Wg) * (X Wu)) Wd.
+ * CPU fp64 oracle for the Gated MLP  Y = (act(X Wg) * (X Wu)) Wd  and its
+ * variants.
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
  * call this file: only the test-suite, the smoke check and the CPU-baseline
@@ -8,13 +9,19 @@
  *
  * What it computes is the plain definition, written out:
  *   - the Gated MLP graph of the paper's Fig. "Gated MLP" (fig:mlp-example,
- *     Section 4.1): X feeds two matmuls (W1 -> silu, W2), their results are
+ *     Section 4.2): X feeds two matmuls (W1 -> silu, W2), their results are
  *     multiplied elementwise, and the product feeds a third matmul with W3.
  *     Here W1 = Wg (gate), W2 = Wu (up), W3 = Wd (down).
  *   - matmul(a, b)[i, j] = sum over k of a[i, k] * b[k, j]  (matmul semantics,
  *     Fig. fig:op-sema in Section 4.2.1, and the granular-operation table
  *     tab:nki-ops in Section 5.1).
  *   - silu(x) = x * sigmoid(x)  (granular-operation table tab:nki-ops).
+ * Variants (the paper's benchmark list in Section 6.1 names SwiGLU and GLU
+ * and a SwiGLU Gated MLP, without formulas; the usual definitions are used):
+ *   - swish_beta(g) = g * sigmoid(beta * g)  (the SwiGLU gate; beta = 1 is
+ *     silu), and sigmoid(g) (the GLU gate) in place of silu;
+ *   - RMSNorm in front (Section 2, the RMSNorm equation): each row x of X is
+ *     replaced by x / sqrt(mean(x^2) + eps) before the two matmuls.
  *
  * Every step is done in IEEE double precision (no fused multiply-add: the
  * build passes -ffp-contract=off).  bf16 inputs are decoded exactly (a bf16
@@ -45,6 +52,31 @@ double gmlp_oracle_silu(double z)
     return z * e / (1.0 + e);
 }
 
+/* sigmoid(z) = 1 / (1 + exp(-z)), with exp(z) / (1 + exp(z)) for z < 0 so
+ * that exp never overflows. */
+double gmlp_oracle_sigmoid(double z)
+{
+    if (z >= 0.0)
+        return 1.0 / (1.0 + exp(-z));
+    double e = exp(z);
+    return e / (1.0 + e);
+}
+
+/* Gate activations (the values of the library's enum gmlp_activation). */
+#define ORACLE_ACT_SILU 0
+#define ORACLE_ACT_SWISH 1
+#define ORACLE_ACT_SIGMOID 2
+
+/* act(g): silu(g), g * sigmoid(beta * g), or sigmoid(g). */
+double gmlp_oracle_gate(double g, int act, double beta)
+{
+    switch (act) {
+    case ORACLE_ACT_SILU: return gmlp_oracle_silu(g);
+    case ORACLE_ACT_SWISH: return g * gmlp_oracle_sigmoid(beta * g);
+    default: return gmlp_oracle_sigmoid(g);
+    }
+}
+
 /* Exact bf16 -> double: the 16 bits are the high half of a binary32. */
 double gmlp_oracle_bf16_to_f64(uint16_t bits)
 {
@@ -64,21 +96,22 @@ static inline double ld_bf16(const uint16_t *p, int64_t i)
 }
 
 /*
- * The two steps of one row, for one element type WT decoded by LD:
+ * The two steps of one row (x already decoded, and normalised if asked),
+ * for weights of one element type WT decoded by LD:
  *
  *   gate_up: for f in [f_lo, f_hi):
  *              G[f] = sum_d x[d] Wg[d, f]      (d ascending)
  *              U[f] = sum_d x[d] Wu[d, f]      (d ascending)
- *              H[f] = silu(G[f]) * U[f]
+ *              H[f] = act(G[f]) * U[f]
  *   down:    for j in [j_lo, j_hi):
  *              Y[j] = sum_f H[f] Wd[f, j]      (f ascending)
  *
  * The column ranges only split work between threads.
  */
 #define DEFINE_ROW_STEPS(SUF, WT, LD)                                           \
-    static int gate_up_##SUF(const WT *x, const WT *Wg, const WT *Wu,           \
+    static int gate_up_##SUF(const double *x, const WT *Wg, const WT *Wu,       \
                              int64_t D, int64_t F, int64_t f_lo,                \
-                             int64_t f_hi, double *h)                           \
+                             int64_t f_hi, int act, double beta, double *h)     \
     {                                                                           \
         int64_t w = f_hi - f_lo;                                                \
         double *g = (double *)calloc((size_t)w, sizeof(double));                \
@@ -89,14 +122,14 @@ static inline double ld_bf16(const uint16_t *p, int64_t i)
             return 1;                                                           \
         }                                                                       \
         for (int64_t d = 0; d < D; ++d) {                                       \
-            double xd = LD(x, d);                                               \
+            double xd = x[d];                                                   \
             for (int64_t j = 0; j < w; ++j) {                                   \
                 g[j] += xd * LD(Wg, d * F + f_lo + j);                          \
                 u[j] += xd * LD(Wu, d * F + f_lo + j);                          \
             }                                                                   \
         }                                                                       \
         for (int64_t j = 0; j < w; ++j)                                         \
-            h[f_lo + j] = gmlp_oracle_silu(g[j]) * u[j];                        \
+            h[f_lo + j] = gmlp_oracle_gate(g[j], act, beta) * u[j];             \
         free(g);                                                                \
         free(u);                                                                \
         return 0;                                                               \
@@ -146,22 +179,45 @@ static int pick_threads(int threads)
 
 /*
  * Entry points.  Arrays are row-major: X [T, D], Wg [D, F], Wu [D, F],
- * Wd [F, D].  rows[n] lists the rows of X to evaluate (NULL means rows
- * 0..n-1).  Outputs: Y [n, D] and, if H is not NULL, H [n, F] (the product
- * silu(G) * U before the down projection).  threads <= 0 uses the OpenMP
- * default.  Returns 0 on success, 1 on a bad argument, 2 on a row index
- * outside [0, T), 3 on allocation failure.
+ * Wd [F, D].  act selects the gate activation (silu, swish_beta, sigmoid),
+ * rms != 0 puts RMSNorm with epsilon eps (>= 0) in front.  rows[n] lists the
+ * rows of X to evaluate (NULL means rows 0..n-1).  Outputs: Y [n, D] and, if
+ * H is not NULL, H [n, F] (the product act(G) * U before the down
+ * projection).  threads <= 0 uses the OpenMP default.  Returns 0 on success,
+ * 1 on a bad argument, 2 on a row index outside [0, T), 3 on allocation
+ * failure.
  */
-#define ORACLE_DRIVER(SUF, WT)                                                  \
+#define ORACLE_DRIVER(SUF, WT, LD)                                              \
     int rc = check_args(X, Wg, Wu, Wd, T, D, F, rows, n, Y);                    \
     if (rc)                                                                     \
         return rc;                                                              \
+    if (act < ORACLE_ACT_SILU || act > ORACLE_ACT_SIGMOID || (rms && !(eps >= 0.0))) \
+        return 1;                                                               \
     if (n == 0)                                                                 \
         return 0;                                                               \
     int nthr = pick_threads(threads);                                           \
     double *h_all = (double *)malloc(sizeof(double) * (size_t)n * (size_t)F);   \
-    if (!h_all)                                                                 \
+    double *x_all = (double *)malloc(sizeof(double) * (size_t)n * (size_t)D);   \
+    if (!h_all || !x_all) {                                                     \
+        free(h_all);                                                            \
+        free(x_all);                                                            \
         return 3;                                                               \
+    }                                                                           \
+    /* The rows of X, decoded; with RMSNorm, x[d] * 1/sqrt(mean(x^2) + eps). */ \
+    for (int64_t r = 0; r < n; ++r) {                                           \
+        int64_t t = rows ? rows[r] : r;                                         \
+        double *xr = x_all + r * D;                                             \
+        for (int64_t d = 0; d < D; ++d)                                         \
+            xr[d] = LD(X, t * D + d);                                           \
+        if (rms) {                                                              \
+            double ss = 0.0;                                                    \
+            for (int64_t d = 0; d < D; ++d)                                     \
+                ss += xr[d] * xr[d];                                            \
+            double inv = 1.0 / sqrt(ss / (double)D + eps);                      \
+            for (int64_t d = 0; d < D; ++d)                                     \
+                xr[d] = xr[d] * inv;                                            \
+        }                                                                       \
+    }                                                                           \
     /* Many rows: one row per task.  Few rows: column ranges per task. */       \
     int64_t fc = n >= nthr ? F : CHUNK, dc = n >= nthr ? D : CHUNK;             \
     int64_t nfc = (F + fc - 1) / fc, ndc = (D + dc - 1) / dc;                   \
@@ -170,9 +226,10 @@ static int pick_threads(int threads)
     for (int64_t task = 0; task < n * nfc; ++task) {                            \
         int64_t r = task / nfc, f_lo = (task % nfc) * fc;                       \
         int64_t f_hi = f_lo + fc < F ? f_lo + fc : F;                           \
-        int64_t t = rows ? rows[r] : r;                                         \
-        fail |= gate_up_##SUF(X + t * D, Wg, Wu, D, F, f_lo, f_hi, h_all + r * F); \
+        fail |= gate_up_##SUF(x_all + r * D, Wg, Wu, D, F, f_lo, f_hi, act, beta, \
+                              h_all + r * F);                                   \
     }                                                                           \
+    free(x_all);                                                                \
     if (fail) {                                                                 \
         free(h_all);                                                            \
         return 3;                                                               \
@@ -188,12 +245,30 @@ static int pick_threads(int threads)
     free(h_all);                                                                \
     return 0;
 
+int gmlp_oracle_variant_rows_bf16(const uint16_t *X, const uint16_t *Wg, const uint16_t *Wu,
+                                  const uint16_t *Wd, int64_t T, int64_t D, int64_t F, int act,
+                                  double beta, int rms, double eps, const int64_t *rows, int64_t n,
+                                  double *Y, double *H, int threads)
+{
+    ORACLE_DRIVER(bf16, uint16_t, ld_bf16)
+}
+
+int gmlp_oracle_variant_rows_f64(const double *X, const double *Wg, const double *Wu,
+                                 const double *Wd, int64_t T, int64_t D, int64_t F, int act,
+                                 double beta, int rms, double eps, const int64_t *rows, int64_t n,
+                                 double *Y, double *H, int threads)
+{
+    ORACLE_DRIVER(f64, double, ld_f64)
+}
+
+/* The SiLU Gated MLP (no RMSNorm): the variant entry points with act = silu. */
 int gmlp_oracle_rows_bf16(const uint16_t *X, const uint16_t *Wg, const uint16_t *Wu,
                           const uint16_t *Wd, int64_t T, int64_t D, int64_t F,
                           const int64_t *rows, int64_t n, double *Y, double *H,
                           int threads)
 {
-    ORACLE_DRIVER(bf16, uint16_t)
+    return gmlp_oracle_variant_rows_bf16(X, Wg, Wu, Wd, T, D, F, ORACLE_ACT_SILU, 1.0, 0, 0.0,
+                                         rows, n, Y, H, threads);
 }
 
 int gmlp_oracle_rows_f64(const double *X, const double *Wg, const double *Wu,
@@ -201,7 +276,8 @@ int gmlp_oracle_rows_f64(const double *X, const double *Wg, const double *Wu,
                          const int64_t *rows, int64_t n, double *Y, double *H,
                          int threads)
 {
-    ORACLE_DRIVER(f64, double)
+    return gmlp_oracle_variant_rows_f64(X, Wg, Wu, Wd, T, D, F, ORACLE_ACT_SILU, 1.0, 0, 0.0,
+                                        rows, n, Y, H, threads);
 }
 
 /*

@@ -3,9 +3,12 @@
 TEST INFRASTRUCTURE ONLY: nothing on the product path may import this module.
 
 The oracle evaluates the plain definition of the SiLU Gated MLP
-(Fig. fig:mlp-example, Section 4.1; matmul semantics Fig. fig:op-sema,
+(Fig. fig:mlp-example, Section 4.2; matmul semantics Fig. fig:op-sema,
 Section 4.2.1; silu(x) = x * sigmoid(x), table tab:nki-ops, Section 5.1)
-in IEEE double precision, on a chosen subset of rows of X.
+in IEEE double precision, on a chosen subset of rows of X, and its variants:
+the gate activation swish_beta(g) = g * sigmoid(beta g) (SwiGLU) or
+sigmoid(g) (GLU), and RMSNorm in front (Section 2: each row x becomes
+x / sqrt(mean(x^2) + eps)).
 """
 from __future__ import annotations
 
@@ -38,6 +41,11 @@ def build(source: str = SOURCE, output: str = LIBRARY, extra_flags: Sequence[str
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
+_D = ctypes.c_double
+_INT = ctypes.c_int
+
+# Gate activations (the values of the library's enum gmlp_activation).
+ACTIVATIONS = {"silu": 0, "swish": 1, "sigmoid": 2}
 
 
 class Oracle:
@@ -50,10 +58,19 @@ class Oracle:
         lib.gmlp_oracle_silu.restype = ctypes.c_double
         lib.gmlp_oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
         lib.gmlp_oracle_bf16_to_f64.restype = ctypes.c_double
+        lib.gmlp_oracle_sigmoid.argtypes = [_D]
+        lib.gmlp_oracle_sigmoid.restype = _D
+        lib.gmlp_oracle_gate.argtypes = [_D, _INT, _D]
+        lib.gmlp_oracle_gate.restype = _D
         for name in ("gmlp_oracle_rows_bf16", "gmlp_oracle_rows_f64"):
             fn = getattr(lib, name)
-            fn.argtypes = [_P, _P, _P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, ctypes.c_int]
-            fn.restype = ctypes.c_int
+            fn.argtypes = [_P, _P, _P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, _INT]
+            fn.restype = _INT
+        for name in ("gmlp_oracle_variant_rows_bf16", "gmlp_oracle_variant_rows_f64"):
+            fn = getattr(lib, name)
+            fn.argtypes = [_P, _P, _P, _P, _I64, _I64, _I64, _INT, _D, _INT, _D, _P, _I64, _P, _P,
+                           _INT]
+            fn.restype = _INT
         lib.gmlp_oracle_down_rows_bf16.argtypes = [_P, _P, _I64, _I64, _I64, _P, _I64, _P,
                                                    ctypes.c_int]
         lib.gmlp_oracle_down_rows_bf16.restype = ctypes.c_int
@@ -68,6 +85,18 @@ class Oracle:
         out = np.vectorize(self.lib.gmlp_oracle_silu, otypes=[np.float64])(arr)
         return float(out) if np.ndim(z) == 0 else out
 
+    def sigmoid(self, z):
+        arr = np.asarray(z, dtype=np.float64)
+        out = np.vectorize(self.lib.gmlp_oracle_sigmoid, otypes=[np.float64])(arr)
+        return float(out) if np.ndim(z) == 0 else out
+
+    def gate(self, g, activation: str = "silu", beta: float = 1.0):
+        """act(g) of the named gate activation, elementwise."""
+        act = ACTIVATIONS[activation]
+        arr = np.asarray(g, dtype=np.float64)
+        out = np.vectorize(lambda v: self.lib.gmlp_oracle_gate(v, act, beta), otypes=[np.float64])(arr)
+        return float(out) if np.ndim(g) == 0 else out
+
     def bf16_to_f64(self, bits):
         arr = np.asarray(bits, dtype=np.uint16)
         return np.vectorize(self.lib.gmlp_oracle_bf16_to_f64, otypes=[np.float64])(arr)
@@ -77,20 +106,24 @@ class Oracle:
 
     # -- the Gated MLP ----------------------------------------------------
     def gated_mlp_rows(self, X, Wg, Wu, Wd, rows: Optional[Sequence[int]] = None,
-                       threads: int = 0, return_h: bool = False):
-        """Rows of Y = (silu(X Wg) * (X Wu)) Wd in double precision.
+                       threads: int = 0, return_h: bool = False, activation: str = "silu",
+                       beta: float = 1.0, rmsnorm: bool = False, eps: float = 1e-6):
+        """Rows of Y = (act(X Wg) * (X Wu)) Wd in double precision.
 
         X [T, D], Wg [D, F], Wu [D, F], Wd [F, D]: either all ``uint16``
         (bf16 bit patterns, decoded exactly) or all floating point (converted
-        to float64).  ``rows`` selects rows of X (default: all).  Returns
+        to float64).  ``rows`` selects rows of X (default: all).  act is
+        silu (default), swish (g * sigmoid(beta g)) or sigmoid; ``rmsnorm``
+        replaces each row x of X by x / sqrt(mean(x^2) + eps) first.  Returns
         Y [len(rows), D] (and H [len(rows), F] if ``return_h``).
         """
         arrays = [np.asarray(a) for a in (X, Wg, Wu, Wd)]
+        plain = activation == "silu" and not rmsnorm
         if all(a.dtype == np.uint16 for a in arrays):
-            fn = self.lib.gmlp_oracle_rows_bf16
+            fn = self.lib.gmlp_oracle_rows_bf16 if plain else self.lib.gmlp_oracle_variant_rows_bf16
             arrays = [np.ascontiguousarray(a, dtype=np.uint16) for a in arrays]
         elif not any(a.dtype == np.uint16 for a in arrays):
-            fn = self.lib.gmlp_oracle_rows_f64
+            fn = self.lib.gmlp_oracle_rows_f64 if plain else self.lib.gmlp_oracle_variant_rows_f64
             arrays = [np.ascontiguousarray(a, dtype=np.float64) for a in arrays]
         else:
             raise TypeError("mixing bf16 bit patterns and floating-point inputs")
@@ -109,9 +142,13 @@ class Oracle:
         n = rows_arr.size
         Y = np.zeros((n, D), dtype=np.float64)
         H = np.zeros((n, F), dtype=np.float64) if return_h else None
-        rc = fn(X.ctypes.data, Wg.ctypes.data, Wu.ctypes.data, Wd.ctypes.data,
-                T, D, F, rows_arr.ctypes.data if n else None, n, Y.ctypes.data,
+        tail = (rows_arr.ctypes.data if n else None, n, Y.ctypes.data,
                 H.ctypes.data if H is not None else None, int(threads))
+        if plain:
+            rc = fn(X.ctypes.data, Wg.ctypes.data, Wu.ctypes.data, Wd.ctypes.data, T, D, F, *tail)
+        else:
+            rc = fn(X.ctypes.data, Wg.ctypes.data, Wu.ctypes.data, Wd.ctypes.data, T, D, F,
+                    ACTIVATIONS[activation], float(beta), int(bool(rmsnorm)), float(eps), *tail)
         if rc != 0:
             raise RuntimeError("oracle returned error code %d" % rc)
         return (Y, H) if return_h else Y
@@ -157,6 +194,7 @@ def silu(z):
     return default_oracle().silu(z)
 
 
-def gated_mlp_rows(X, Wg, Wu, Wd, rows=None, threads: int = 0, return_h: bool = False):
+def gated_mlp_rows(X, Wg, Wu, Wd, rows=None, threads: int = 0, return_h: bool = False,
+                   **variant):
     return default_oracle().gated_mlp_rows(X, Wg, Wu, Wd, rows=rows, threads=threads,
-                                           return_h=return_h)
+                                           return_h=return_h, **variant)

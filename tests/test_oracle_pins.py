@@ -12,7 +12,10 @@ Definitions pinned (from the paper):
   * matmul as a sum of products, Fig. fig:op-sema (Section 4.2.1);
   * silu(x) = x * sigmoid(x), table tab:nki-ops (Section 5.1);
   * the illegal "silu past multiply" swap (Section 5.1, Examples) is one of
-    the planted mutants.
+    the planted mutants;
+  * the variants: gate activations swish_beta(g) = g * sigmoid(beta g) and
+    sigmoid(g) (the paper's SwiGLU / GLU benchmarks, Section 6.1, usual
+    definitions), and RMSNorm in front (the RMSNorm equation, Section 2).
 """
 from __future__ import annotations
 
@@ -275,6 +278,132 @@ PINS = [
 ]
 
 
+# ---------------------------------------------------------------- variants ----
+def _logit_ps():
+    ps = []
+    with open(os.path.join(GOLDEN, "silu_logit_points.txt")) as fh:
+        for line in fh:
+            line = line.split("#")[0].strip()
+            if line:
+                ps.append(Fraction(line))
+    return ps
+
+
+def pin_sigmoid_logit_points(orc):
+    # sigmoid(ln(p / (1 - p))) = p exactly; the GLU gate.
+    for p in _logit_ps():
+        x = math.log(p / (1 - p))
+        want = float(p)
+        got = orc.gate(x, "sigmoid")
+        assert abs(got - want) <= 2.3e-16 * (4 + 2 * abs(x)) * abs(want), (p, got)
+        assert orc.sigmoid(x) == got
+
+
+def pin_swish_logit_points(orc):
+    # beta * x = ln(p / (1 - p))  =>  swish_beta(x) = x * p.
+    for beta in (0.5, 1.702, 3.0):
+        for p in _logit_ps():
+            x = math.log(p / (1 - p)) / beta
+            want = x * float(p)
+            got = orc.gate(x, "swish", beta)
+            assert abs(got - want) <= 2.3e-16 * (6 + 2 * abs(beta * x)) * abs(want), (beta, p, got)
+
+
+def pin_swish_beta_zero_is_bilinear(orc):
+    # swish_0(g) = g / 2: Y = ((X Wg) / 2 * (X Wu)) Wd, a library matmul.
+    X, Wg, Wu, Wd = _rand_problem(41, 3, 16, 24)
+    want = (0.5 * (X @ Wg) * (X @ Wu)) @ Wd
+    got = orc.gated_mlp_rows(X, Wg, Wu, Wd, activation="swish", beta=0.0)
+    ok, worst = _close(got, want, 1e-12, 1e-14)
+    assert ok, worst
+
+
+def pin_swish_large_beta_is_relu(orc):
+    # beta -> inf: swish_beta(g) -> max(g, 0) (error below g e^{-beta |g|}).
+    X, Wg, Wu, Wd = _rand_problem(42, 3, 16, 24)
+    G = X @ Wg
+    assert np.min(np.abs(G)) > 1e-3
+    want = (np.maximum(G, 0.0) * (X @ Wu)) @ Wd
+    got = orc.gated_mlp_rows(X, Wg, Wu, Wd, activation="swish", beta=1e6)
+    ok, worst = _close(got, want, 1e-10, 1e-12)
+    assert ok, worst
+
+
+def pin_glu_library(orc):
+    # sigmoid gate against numpy matmul and scipy's logistic function.
+    X, Wg, Wu, Wd = _rand_problem(43, 4, 32, 40, scale=2.0)
+    want = (expit(X @ Wg) * (X @ Wu)) @ Wd
+    got = orc.gated_mlp_rows(X, Wg, Wu, Wd, activation="sigmoid")
+    ok, worst = _close(got, want, 1e-12, 1e-13)
+    assert ok, worst
+
+
+def pin_glu_zero_gate_halves_up(orc):
+    # Wg = 0: sigmoid(0) = 1/2 exactly, so Y = ((X Wu) / 2) Wd.
+    X, Wg, Wu, Wd = _rand_problem(44, 3, 16, 24)
+    want = (0.5 * (X @ Wu)) @ Wd
+    got = orc.gated_mlp_rows(X, np.zeros_like(Wg), Wu, Wd, activation="sigmoid")
+    ok, worst = _close(got, want, 1e-12, 1e-14)
+    assert ok, worst
+
+
+def pin_variants_brute_force(orc):
+    X, Wg, Wu, Wd = _rand_problem(45, 2, 5, 7, scale=1.5)
+    lists = [a.tolist() for a in (X, Wg, Wu, Wd)]
+    for kw in ({"activation": "swish", "beta": 1.7}, {"activation": "sigmoid"},
+               {"rmsnorm": True, "eps": 1e-3}, {"activation": "swish", "beta": 0.3,
+                                                "rmsnorm": True, "eps": 0.25}):
+        want = np.array(oracle.brute_gated_mlp(*lists, **kw))
+        got = orc.gated_mlp_rows(X, Wg, Wu, Wd, **kw)
+        ok, worst = _close(got, want, 1e-12, 1e-14)
+        assert ok, (kw, worst)
+
+
+def pin_rmsnorm_unit_rows_are_unchanged(orc):
+    # Rows of +-1 have mean(x^2) = 1 exactly: with eps = 0 RMSNorm is the
+    # identity, so the result equals the plain Gated MLP bit for bit.
+    r = _rng(46)
+    X = np.where(r.standard_normal((4, 32)) > 0, 1.0, -1.0)
+    _, Wg, Wu, Wd = _rand_problem(46, 4, 32, 24)
+    plain = orc.gated_mlp_rows(X, Wg, Wu, Wd)
+    normed = orc.gated_mlp_rows(X, Wg, Wu, Wd, rmsnorm=True, eps=0.0)
+    assert np.array_equal(plain, normed)
+
+
+def pin_rmsnorm_scale_invariant(orc):
+    # RMSNorm(c x) = RMSNorm(x) for c > 0 when eps = 0.
+    X, Wg, Wu, Wd = _rand_problem(47, 3, 32, 24)
+    a = orc.gated_mlp_rows(X, Wg, Wu, Wd, rmsnorm=True, eps=0.0)
+    b = orc.gated_mlp_rows(X * 37.0, Wg, Wu, Wd, rmsnorm=True, eps=0.0)
+    ok, worst = _close(b, a, 1e-13, 1e-15)
+    assert ok, worst
+    assert not np.allclose(a, orc.gated_mlp_rows(X, Wg, Wu, Wd), rtol=1e-3)
+
+
+def pin_rmsnorm_closed_form_eps(orc):
+    # A row of equal values a: mean(x^2) = a^2, so RMSNorm gives
+    # a / sqrt(a^2 + eps); with a = 1, eps = 3 that is exactly 1/2.
+    _, Wg, Wu, Wd = _rand_problem(48, 1, 16, 24)
+    X = np.ones((1, 16))
+    want = orc.gated_mlp_rows(0.5 * X, Wg, Wu, Wd)
+    got = orc.gated_mlp_rows(X, Wg, Wu, Wd, rmsnorm=True, eps=3.0)
+    assert np.array_equal(got, want)
+
+
+PINS += [
+    pin_sigmoid_logit_points,
+    pin_swish_logit_points,
+    pin_swish_beta_zero_is_bilinear,
+    pin_swish_large_beta_is_relu,
+    pin_glu_library,
+    pin_glu_zero_gate_halves_up,
+    pin_variants_brute_force,
+    pin_rmsnorm_unit_rows_are_unchanged,
+    pin_rmsnorm_scale_invariant,
+    pin_rmsnorm_closed_form_eps,
+]
+
+
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
 def test_pin(orc, pin):
     pin(orc)
@@ -290,13 +419,13 @@ def test_brute_force_handles_large_negative_gate():
 # occur exactly once in the source.
 MUTANTS = [
     ("silu moved past the multiply (the illegal swap of Section 5.1)",
-     "h[f_lo + j] = gmlp_oracle_silu(g[j]) * u[j];",
-     "h[f_lo + j] = gmlp_oracle_silu(g[j] * u[j]);"),
+     "h[f_lo + j] = gmlp_oracle_gate(g[j], act, beta) * u[j];",
+     "h[f_lo + j] = gmlp_oracle_gate(g[j] * u[j], act, beta);"),
     ("gate and up swapped",
-     "h[f_lo + j] = gmlp_oracle_silu(g[j]) * u[j];",
-     "h[f_lo + j] = gmlp_oracle_silu(u[j]) * g[j];"),
-    ("silu dropped",
-     "h[f_lo + j] = gmlp_oracle_silu(g[j]) * u[j];",
+     "h[f_lo + j] = gmlp_oracle_gate(g[j], act, beta) * u[j];",
+     "h[f_lo + j] = gmlp_oracle_gate(u[j], act, beta) * g[j];"),
+    ("gate activation dropped",
+     "h[f_lo + j] = gmlp_oracle_gate(g[j], act, beta) * u[j];",
      "h[f_lo + j] = g[j] * u[j];"),
     ("sigmoid argument sign flipped",
      "return z / (1.0 + exp(-z));",
@@ -314,11 +443,32 @@ MUTANTS = [
      "for (int64_t d = 0; d < D; ++d) {",
      "for (int64_t d = 0; d + 1 < D; ++d) {"),
     ("requested row list ignored",
-     "gate_up_##SUF(X + t * D,",
-     "gate_up_##SUF(X + r * D,"),
+     "xr[d] = LD(X, t * D + d);",
+     "xr[d] = LD(X, r * D + d);"),
     ("bf16 decoded with the wrong shift",
      "uint32_t u = (uint32_t)p[i] << 16;",
      "uint32_t u = (uint32_t)p[i] << 15;"),
+    ("swish ignores beta",
+     "case ORACLE_ACT_SWISH: return g * gmlp_oracle_sigmoid(beta * g);",
+     "case ORACLE_ACT_SWISH: return g * gmlp_oracle_sigmoid(g);"),
+    ("GLU gate computes silu",
+     "default: return gmlp_oracle_sigmoid(g);",
+     "default: return gmlp_oracle_silu(g);"),
+    ("sigmoid sign flipped",
+     "return 1.0 / (1.0 + exp(-z));",
+     "return 1.0 / (1.0 + exp(z));"),
+    ("sigmoid negative branch wrong",
+     "return e / (1.0 + e);",
+     "return 1.0 / (1.0 + e);"),
+    ("RMSNorm eps dropped",
+     "double inv = 1.0 / sqrt(ss / (double)D + eps);",
+     "double inv = 1.0 / sqrt(ss / (double)D);"),
+    ("RMSNorm sum instead of mean",
+     "double inv = 1.0 / sqrt(ss / (double)D + eps);",
+     "double inv = 1.0 / sqrt(ss + eps);"),
+    ("RMSNorm scale not applied",
+     "xr[d] = xr[d] * inv;",
+     "xr[d] = xr[d] * 1.0;"),
 ]
 
 
