@@ -2,6 +2,7 @@
 """Benchmark of the MI355X SiLU Gated MLP, Y = (silu(X Wg) * (X Wu)) Wd.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--variant silu|swiglu|glu|rmsnorm|rmsnorm_swiglu]
 
 One step is one full pass of the hot path (one fused persistent GEMV kernel
 for T <= 7, else a gate/up kernel and a down kernel) over one batch of
@@ -25,6 +26,9 @@ shape) with:
              peak (8 TB/s HBM, 2.5 PFLOP/s dense bf16);
   cpu_baseline  the CPU fp64 oracle on this host's cores, on a bounded
              sample of the same workload, scaled to the same unit.
+--variant selects a member of the Gated MLP family (default: the SiLU Gated
+MLP): swiglu = swish gate with beta 1.702, glu = sigmoid gate, rmsnorm =
+RMSNorm of X in front (eps 1e-6), rmsnorm_swiglu = both.
 Only one GPU is used: --gpus above 1 exits with a message.
 """
 from __future__ import annotations
@@ -45,6 +49,14 @@ RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)  # ~312 FLOP/B
 MALL_DEFEAT_BYTES = 1.1e9      # rotate weights over at least this many bytes
 COPY_BYTES = 256 << 20         # size of the calibration copy
 HERE = os.path.dirname(os.path.abspath(__file__))
+# Members of the Gated MLP family: oracle/binding keyword arguments.
+VARIANTS = {
+    "silu": {},
+    "swiglu": {"activation": "swish", "beta": 1.702},
+    "glu": {"activation": "sigmoid"},
+    "rmsnorm": {"rmsnorm": True, "eps": 1e-6},
+    "rmsnorm_swiglu": {"activation": "swish", "beta": 1.702, "rmsnorm": True, "eps": 1e-6},
+}
 PROFILES = os.path.join(HERE, "profiles")
 CSRC = os.path.join(HERE, "paper_2606_26344_amd", "csrc")
 
@@ -83,6 +95,8 @@ def parse_args(argv=None):
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="decode",
                    help="decode | tiny | small_batch | prefill | large_prefill | all")
+    p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
+                   help="member of the Gated MLP family (default: the SiLU Gated MLP)")
     p.add_argument("--copies", type=int, default=0,
                    help="weight copies to rotate through (0: enough to exceed 1.1 GB "
                         "for memory-bound shapes, 1 otherwise)")
@@ -112,7 +126,7 @@ def gate_up_algorithmic(T, D, F):
     return 2.0 * (2.0 * D * F + T * D + T * F), 4.0 * T * D * F
 
 
-def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s):
+def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s, variant=None):
     import numpy as np
 
     import oracle
@@ -123,14 +137,15 @@ def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s):
     threads = orc.max_threads()
     # Calibrate on one row, then size the sample to fill the time budget.
     t0 = time.perf_counter()
-    orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=[0])
+    variant = variant or {}
+    orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=[0], **variant)
     t_row = max(time.perf_counter() - t0, 1e-6)
     n = int(max(1, min(T, budget_s // t_row)))
     rows = np.linspace(0, T - 1, n).round().astype(np.int64) if n < T else None
     reps = 1 if n < T else int(max(1, min(100000, budget_s // (t_row * T))))
     t0 = time.perf_counter()
     for _ in range(reps):
-        orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows)
+        orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows, **variant)
     t_total = time.perf_counter() - t0
     rows_done = (T if rows is None else n)
     t_full = (t_total / reps) * T / rows_done  # seconds per full step
@@ -181,14 +196,21 @@ def run_workload(name, args):
     xp, yp, hp, wsp = P(x.data_ptr()), P(y.data_ptr()), P(h.data_ptr()), P(ws.buffer.data_ptr())
     wp = [tuple(P(t.data_ptr()) for t in s) for s in wsets]
     auto = gmlp.PATH_AUTO
+    variant = VARIANTS[args.variant]
+    vargs = gmlp._variant(variant.get("activation", "silu"), variant.get("beta", 1.0),
+                          variant.get("rmsnorm", False), variant.get("eps", 0.0))
 
     def step(i):
         g, u, d = wp[i % copies]
-        return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, auto, wsp, ws.nbytes, st)
+        if not variant:
+            return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, auto, wsp, ws.nbytes, st)
+        return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, auto, wsp, ws.nbytes, st)
 
     def gate_up_only(i):
         g, u, _ = wp[i % copies]
-        return lib.gmlp_gate_up_ws(xp, g, u, hp, T, D, F, auto, wsp, ws.nbytes, st)
+        if not variant:
+            return lib.gmlp_gate_up_ws(xp, g, u, hp, T, D, F, auto, wsp, ws.nbytes, st)
+        return lib.gmlp_gate_up_variant(xp, g, u, hp, T, D, F, *vargs, auto, wsp, ws.nbytes, st)
 
     def down_only(i):
         _, _, d = wp[i % copies]
@@ -255,8 +277,10 @@ def run_workload(name, args):
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "%s: T=%d, D=%d, F=%d%s" % (
-                name, T, D, F, ", X rows at unit RMS" if w.unit_rms_rows else ""),
+            "workload": "%s%s: T=%d, D=%d, F=%d%s" % (
+                name, "" if args.variant == "silu" else " (%s Gated MLP)" % args.variant, T, D, F,
+                ", X rows at unit RMS" if w.unit_rms_rows else ""),
+            "variant": dict({"name": args.variant}, **variant),
             "T": T, "D": D, "F": F,
             "path": path,
             "kernels": [{"name": k, "grid": g, "block": b, "k_splits": sp} for k, g, b, sp in plan],
@@ -298,7 +322,7 @@ def run_workload(name, args):
         result["copy_calibration_bytes"] = COPY_BYTES
         del src, dst
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds, variant)
     del wsets, x, y, h, ws
     torch.cuda.empty_cache()
     return result

@@ -64,6 +64,17 @@ enum gmlp_path {
     GMLP_PATH_MFMA = 2, /* MFMA GEMM kernels (any T) */
 };
 
+/*
+ * Gate activations of the Gated MLP family, H = act(X Wg) * (X Wu).  The
+ * paper benchmarks a SiLU and a SwiGLU Gated MLP and a GLU operator (Section
+ * 6.1) without spelling them out; the usual definitions are used:
+ */
+enum gmlp_activation {
+    GMLP_ACT_SILU = 0,    /* silu(g) = g * sigmoid(g)  (table tab:nki-ops, Section 5.1) */
+    GMLP_ACT_SWISH = 1,   /* swish_beta(g) = g * sigmoid(beta * g)  (SwiGLU; beta = 1 is silu) */
+    GMLP_ACT_SIGMOID = 2, /* sigmoid(g)  (GLU) */
+};
+
 /* Library version, GMLP_VERSION of the build. */
 int gmlp_version(void);
 
@@ -88,7 +99,9 @@ int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg
  * text: one line per kernel, in launch order,
  *     "<kernel> grid=<blocks> block=<threads> k_splits=<n>\n"
  * with <kernel> as a profiler names it without the namespace (for example
- * "gemv_splitk_kernel<1, 2, 0>").  NUL-terminated, truncated to `bytes`
+ * "gemv_splitk_kernel<1, 2, 0, false>"), for the SiLU Gated MLP (the
+ * variants of gmlp_forward_variant use the same plan; RMSNorm adds its
+ * row-scale kernel on the MFMA path).  NUL-terminated, truncated to `bytes`
  * (which must be > 0).  Host-only: makes no HIP call.  Nothing for T == 0.
  * GMLP_OK, or INVALID_ARG / UNSUPPORTED for a bad shape, path or buffer.
  */
@@ -132,6 +145,25 @@ int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *W
                     size_t ws_bytes, void *stream);
 
 /*
+ * A member of the Gated MLP family, with a caller workspace as for
+ * gmlp_forward_ex:
+ *     Y = (act(Xn Wg) * (Xn Wu)) Wd,
+ * act = `activation` (enum gmlp_activation; `beta` is used by GMLP_ACT_SWISH
+ * only and must be finite), and Xn = X, or with rmsnorm = 1 the RMSNorm of
+ * X (the equation of Section 2, no gain): each row x becomes
+ * x / sqrt(mean(x^2) + eps), eps finite and >= 0.  The normalisation is
+ * never materialised: by the paper's reorder of the multiply past the
+ * matmul, G and U are computed from X and scaled per row before act.  With
+ * GMLP_ACT_SILU and rmsnorm = 0 this is gmlp_forward_ex, bit for bit.
+ * INVALID_ARG for an unknown activation, a non-finite beta or a bad
+ * rmsnorm/eps; otherwise as gmlp_forward_ex.
+ */
+int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                         int64_t T, int64_t D, int64_t F, int activation, float beta,
+                         int rmsnorm, float eps, int path, void *workspace, size_t ws_bytes,
+                         void *stream);
+
+/*
  * First half of the graph alone (the paper's "MM+MM+SiLU+Mul" kernel):
  * H = bf16(silu(X Wg) * (X Wu)), H [T, F].  Allocates its scratch
  * stream-ordered on `stream`.
@@ -155,6 +187,12 @@ int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int6
 int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T,
                     int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes,
                     void *stream);
+
+/* The gate/up step of gmlp_forward_variant alone: H = bf16(act(Xn Wg) * (Xn Wu)),
+ * with the same activation, beta, rmsnorm and eps arguments. */
+int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H, int64_t T,
+                         int64_t D, int64_t F, int activation, float beta, int rmsnorm,
+                         float eps, int path, void *workspace, size_t ws_bytes, void *stream);
 int gmlp_down_ws(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D,
                  int path, void *workspace, size_t ws_bytes, void *stream);
 

@@ -15,7 +15,7 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
 // What the last step of a kernel writes.
 enum Epilogue {
-    EPI_SILU_MUL = 0, // out = bf16(silu(acc0) * acc1)   (H of the gate/up step)
+    EPI_GATE_MUL = 0, // out = bf16(act(acc0) * acc1)    (H of the gate/up step)
     EPI_STORE = 1,    // out = bf16(acc0)                (Y of the down step)
 };
 
@@ -90,6 +90,23 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __builtin_bit_cast
 __device__ __forceinline__ float silu(float z)
 {
     return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
+
+// Gate activations of the Gated MLP family (values of enum gmlp_activation).
+enum Activation {
+    ACT_SILU = 0,    // silu(g)                    the SiLU Gated MLP
+    ACT_SWISH = 1,   // g * sigmoid(beta * g)      the SwiGLU Gated MLP
+    ACT_SIGMOID = 2, // sigmoid(g)                 the GLU Gated MLP
+};
+
+// act(g) for a block-uniform activation.
+__device__ __forceinline__ float gate_act(float g, int act, float beta)
+{
+    if (act == ACT_SILU)
+        return silu(g);
+    if (act == ACT_SWISH)
+        return g * __builtin_amdgcn_rcpf(1.0f + __expf(-(beta * g)));
+    return __builtin_amdgcn_rcpf(1.0f + __expf(-g));
 }
 
 // Hardware places consecutive workgroups round-robin on the 8 XCDs (each with

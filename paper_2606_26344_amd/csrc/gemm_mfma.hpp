@@ -3,12 +3,15 @@
 // One template computes   C[n, m] = sum_k act[n, k] * W[k, m]
 // for row-major activations act [N, K] (K contiguous) and weights W [K, M]
 // (M contiguous), i.e. the matmuls of the Gated MLP graph (Fig.
-// fig:mlp-example, Section 4.1) with N = tokens.  Two instantiations matter:
+// fig:mlp-example, Section 4.2) with N = tokens.  Two instantiations matter:
 //
 //   * dual-B gate/up:  NW = 2 weights (Wg, Wu) share every staged tile of X
 //     (the paper's fusion of independent matmuls into one loop nest,
-//     Section 4.5), and the epilogue writes H = bf16(silu(G) * U) straight
-//     from the fp32 accumulators; G and U never leave registers.
+//     Section 4.5), and the epilogue writes H = bf16(act(r G) * (r U))
+//     straight from the fp32 accumulators (act = silu, swish_beta or
+//     sigmoid; r = the row's RMSNorm scale if one is given, else 1: the
+//     paper's reorder of the RMSNorm multiply past the matmul, Section 2);
+//     G and U never leave registers.
 //   * down:            NW = 1 (Wd), epilogue writes Y = bf16(H Wd).
 //
 // Data flow per k-step of BK:
@@ -58,6 +61,11 @@ struct GemmParams {
     int splits;
     int tiles_m, tiles_n;
     int group_m; // consecutive blocks sweep group_m column tiles before the next token tile
+    // Gate/up epilogue: activation (enum Activation), swish slope, and the
+    // per-token RMSNorm scales [N] (nullptr: none).
+    int activation;
+    float beta;
+    const float *rrms;
 };
 
 template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_, int BK_>
@@ -463,7 +471,14 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                             acc[w][mi][ni][4 * j + e] = sum[((w * TM + mi) * TN + ni) * 4 + j][e];
     }
 
-    // ---- epilogue: fp32 -> (silu(G) * U) -> bf16, 8-byte row-major stores -----
+    // ---- epilogue: fp32 -> act(r G) * (r U) -> bf16, 8-byte row-major stores --
+    float rs[TN];
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+        rs[ni] = EPI == EPI_GATE_MUL && p.rrms && t < N ? p.rrms[t] : 1.0f;
+    }
+    const bool scaled = EPI == EPI_GATE_MUL && p.rrms;
 #pragma unroll
     for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
@@ -476,10 +491,16 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        if constexpr (EPI == EPI_SILU_MUL)
-                            v[e] = silu(acc[0][mi][ni][4 * j + e]) * acc[NW - 1][mi][ni][4 * j + e];
-                        else
+                        if constexpr (EPI == EPI_GATE_MUL) {
+                            float g = acc[0][mi][ni][4 * j + e], u = acc[NW - 1][mi][ni][4 * j + e];
+                            if (scaled) {
+                                g *= rs[ni];
+                                u *= rs[ni];
+                            }
+                            v[e] = gate_act(g, p.activation, p.beta) * u;
+                        } else {
                             v[e] = acc[0][mi][ni][4 * j + e];
+                        }
                     }
                     u32x2 packed = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
                     *(u32x2 *)(p.out + (size_t)t * M + f) = packed;

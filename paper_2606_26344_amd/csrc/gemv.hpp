@@ -20,8 +20,9 @@
 //   The result is therefore bitwise reproducible run to run.
 //
 // The gate/up kernel (NW = 2) streams Wg and Wu together and its last block
-// applies H = bf16(silu(G) * U); the down kernel (NW = 1) streams Wd and writes
-// Y = bf16(H Wd).
+// applies H = bf16(act(G) * U) (act = silu, swish_beta or sigmoid; with
+// RMSNorm, G and U are first scaled by the row's r); the down kernel (NW = 1)
+// streams Wd and writes Y = bf16(H Wd).
 #pragma once
 
 #include "common.hpp"
@@ -40,6 +41,13 @@ struct GemvParams {
     int splits;
     int strips;
     int strip_lanes; // lanes per row (8 columns each, <= 32): strip width 8 * strip_lanes
+    // Gate/up epilogue: activation (enum Activation) and swish slope.
+    int activation;
+    float beta;
+    // RMSNorm (gate/up kernel with RMS = true): eps, and per-split sums of
+    // squares of the activations [splits][NT] fp32 when splits > 1.
+    float eps;
+    float *ssq;
 };
 
 constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
@@ -54,17 +62,25 @@ template <int NT>
 constexpr int gemv_depth() { return 2; }
 
 
-// LDS of one block: per-wave column sums, last-block flag.
+// LDS of one block: per-wave column sums, per-wave sums of squares of the
+// activations (RMSNorm), last-block flag.
 template <int NT, int NW>
 struct GemvShared {
     float red[4][NW][NT][kGemvMaxStrip];
+    float ssq[4][NT];
     int last;
 };
 
 // One work item (strip, split) of a GEMV step, run by the whole block.
-template <int NT, int NW, int EPI>
+// RMS (gate/up only): the activations are RMSNorm-ed rows.  By the paper's
+// reorder of the RMSNorm multiply past the matmul (Section 2), the block
+// streams the raw rows, adds up the squares of the activations it loads
+// anyway, and the last block of the strip scales G and U by
+// r = 1 / sqrt(sum(x^2) / K + eps) before the activation.
+template <int NT, int NW, int EPI, bool RMS>
 __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh)
 {
+    static_assert(!RMS || EPI == EPI_GATE_MUL, "RMSNorm belongs to the gate/up step");
     constexpr int RG = 8; // row groups per block
     constexpr int U = gemv_batch_rows<NT>();
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -143,6 +159,7 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
         load_batch(ring[i], i); // past the split if i >= nb (never accumulated)
 
     float acc[NW][NT][8];
+    float ssq[NT]; // RMS: this row group's sum of x^2 per token
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
@@ -150,6 +167,9 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 acc[w][t][e] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+        ssq[t] = 0.0f;
 
     {
         auto fma_batch = [&](const Batch &bt, int b) __attribute__((always_inline)) {
@@ -160,6 +180,8 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
                         const float x = u & 1 ? bf16_hi(bt.x[t][u / 2]) : bf16_lo(bt.x[t][u / 2]);
+                        if constexpr (RMS)
+                            ssq[t] += x * x;
 #pragma unroll
                         for (int w = 0; w < NW; ++w)
 #pragma unroll
@@ -203,6 +225,15 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 acc[w][t][e] += __shfl_xor(acc[w][t][e], 32);
+    if constexpr (RMS) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            ssq[t] += __shfl_xor(ssq[t], 32);
+        if (lane == 0)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                sh.ssq[wave][t] = ssq[t];
+    }
     if (lane < 32) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
@@ -226,6 +257,11 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
         for (int t = 0; t < NT; ++t)
             v[w][t] = ((sh.red[0][w][t][tid] + sh.red[1][w][t][tid]) + sh.red[2][w][t][tid]) +
                       sh.red[3][w][t][tid];
+    float ss[NT]; // RMS: the block's (then the whole row's) sum of x^2 per token
+    if constexpr (RMS)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            ss[t] = ((sh.ssq[0][t] + sh.ssq[1][t]) + sh.ssq[2][t]) + sh.ssq[3][t];
 
     if (p.splits > 1) {
         // Per-item sums go out with device-coherent stores; once they have
@@ -240,6 +276,10 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                     __hip_atomic_store(&p.partial[(((size_t)split * NW + w) * NT + t) * M + m], v[w][t],
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
+        if constexpr (RMS)
+            if (tid < NT)
+                __hip_atomic_store(&p.ssq[split * NT + tid], ss[tid], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
         wait_vmcnt<0>();
         __syncthreads();
         if (tid == 0) {
@@ -252,6 +292,34 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
             return;
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (RMS) {
+            // The whole row's sum of squares, splits added in order; the
+            // loads of 32 / NT splits are in flight at once.
+            constexpr int C = NT >= 32 ? 1 : 32 / NT;
+            float tot[NT];
+            for (int s0 = 0; s0 < p.splits; s0 += C) {
+                float x[C][NT];
+#pragma unroll
+                for (int u = 0; u < C; ++u)
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        const int sp = s0 + u;
+                        x[u][t] = sp == split ? ss[t]
+                                  : sp < p.splits ? __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED,
+                                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                                  : 0.0f;
+                    }
+#pragma unroll
+                for (int u = 0; u < C; ++u)
+                    if (s0 + u < p.splits)
+#pragma unroll
+                        for (int t = 0; t < NT; ++t)
+                            tot[t] = s0 + u == 0 ? x[u][t] : tot[t] + x[u][t];
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                ss[t] = tot[t];
+        }
         if (mvalid) {
             // Sum the splits in order 0, 1, 2, ...; the loads of C splits
             // (about 32 values per thread) are in flight at once.
@@ -295,22 +363,29 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             float y;
-            if constexpr (EPI == EPI_SILU_MUL)
-                y = silu(v[0][t]) * v[NW - 1][t];
-            else
+            if constexpr (EPI == EPI_GATE_MUL) {
+                float g = v[0][t], u = v[NW - 1][t];
+                if constexpr (RMS) {
+                    const float r = 1.0f / __builtin_sqrtf(ss[t] / (float)K + p.eps);
+                    g *= r;
+                    u *= r;
+                }
+                y = gate_act(g, p.activation, p.beta) * u;
+            } else {
                 y = v[0][t];
+            }
             p.out[(size_t)t * M + m] = __builtin_bit_cast(uint16_t, (__bf16)y);
         }
     }
 }
 
 // At most 256 VGPRs per lane: two blocks per CU stay resident.
-template <int NT, int NW, int EPI>
+template <int NT, int NW, int EPI, bool RMS = false>
 __global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void gemv_splitk_kernel(GemvParams p)
 {
     __shared__ GemvShared<NT, NW> sh;
-    gemv_item<NT, NW, EPI>(p, blockIdx.x, sh);
+    gemv_item<NT, NW, EPI, RMS>(p, blockIdx.x, sh);
 }
 
 } // namespace gmlp

@@ -4,18 +4,20 @@
 // configuration for a shape (the library's static analogue of the paper's
 // empirical per-shape selection, Section 4.6), workspace layout and launches.
 // Every arithmetic step of the Gated MLP runs in the kernels of
-// gemm_mfma.hpp and gemv.hpp.
+// gemm_mfma.hpp, gemv.hpp and rmsnorm.hpp.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 #include <string>
 
 #include "gmlp.h"
 #include "gemm_mfma.hpp"
 #include "gemv.hpp"
+#include "rmsnorm.hpp"
 
 using namespace gmlp;
 
@@ -85,8 +87,16 @@ struct Plan {
 
 
 struct Layout {
-    size_t counters_off = 0, h_off = 0, partial_off = 0, total = 0;
+    size_t counters_off = 0, h_off = 0, partial_off = 0, rrms_off = 0, total = 0;
     int counters = 0; // most arrival counters any path uses for this shape
+};
+
+// Which member of the Gated MLP family a call computes.
+struct Variant {
+    int act = GMLP_ACT_SILU;
+    float beta = 1.0f;
+    bool rms = false; // RMSNorm in front
+    float eps = 0.0f;
 };
 
 // Split K so that at most `target` blocks run (the small-T kernels hold one
@@ -175,7 +185,8 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.splits = (int)cdiv(K, rows);
     s.blocks = s.strips * s.splits;
     s.counters = s.splits > 1 ? s.strips : 0;
-    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * nw * N * M * sizeof(float) : 0;
+    // Per-split column sums, then (gate/up) per-split sums of squares of X.
+    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * (nw * N * M + N) * sizeof(float) : 0;
 }
 
 Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
@@ -219,7 +230,8 @@ Layout make_layout(int64_t T, int64_t D, int64_t F)
     l.h_off = kCounterBytes;
     l.counters = counters;
     l.partial_off = l.h_off + align_up((size_t)T * F * 2);
-    l.total = l.partial_off + align_up(partial);
+    l.rrms_off = l.partial_off + align_up(partial);
+    l.total = l.rrms_off + align_up((size_t)T * sizeof(float));
     return l;
 }
 
@@ -284,7 +296,7 @@ int hip_check(hipError_t e, const char *what)
 
 template <class S, int EPI, bool SPLIT>
 int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                uint8_t *ws, const Layout &l, hipStream_t stream)
+                uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, hipStream_t stream)
 {
     GemmParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -301,6 +313,9 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.tiles_m = s.tiles_m;
     p.tiles_n = s.tiles_n;
     p.group_m = s.group_m;
+    p.activation = v.act;
+    p.beta = v.beta;
+    p.rrms = rrms;
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
     if (s.partial_bytes > (size_t)kNumRecords)
@@ -311,7 +326,7 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
 }
 
 GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                       uint8_t *ws, const Layout &l)
+                       uint8_t *ws, const Layout &l, const Variant &v)
 {
     GemvParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -326,44 +341,65 @@ GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void
     p.splits = s.splits;
     p.strips = s.strips;
     p.strip_lanes = s.strip_lanes;
+    p.activation = v.act;
+    p.beta = v.beta;
+    p.eps = v.eps;
+    // Sums of squares follow the column sums of every split.
+    p.ssq = p.partial + (size_t)s.splits * 2 * s.N * s.M;
     return p;
 }
 
-template <int NT, int NW, int EPI>
+template <int NT, int NW, int EPI, bool RMS>
 int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                   uint8_t *ws, const Layout &l, hipStream_t stream)
+                   uint8_t *ws, const Layout &l, const Variant &v, hipStream_t stream)
 {
-    const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l);
-    hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI>), dim3(s.blocks), dim3(kGemvThreads), 0,
+    const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l, v);
+    hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI, RMS>), dim3(s.blocks), dim3(kGemvThreads), 0,
                        stream, p);
     return hip_check(hipGetLastError(), "GEMV launch");
 }
 
-template <int NW, int EPI>
+template <int NW, int EPI, bool RMS>
 int launch_gemv(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                uint8_t *ws, const Layout &l, hipStream_t stream)
+                uint8_t *ws, const Layout &l, const Variant &v, hipStream_t stream)
 {
     switch (s.N) {
-    case 1: return launch_gemv_nt<1, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 2: return launch_gemv_nt<2, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 3: return launch_gemv_nt<3, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 4: return launch_gemv_nt<4, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 5: return launch_gemv_nt<5, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 6: return launch_gemv_nt<6, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 7: return launch_gemv_nt<7, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
-    case 8: return launch_gemv_nt<8, NW, EPI>(s, w0, w1, act, out, ws, l, stream);
+    case 1: return launch_gemv_nt<1, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 2: return launch_gemv_nt<2, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 3: return launch_gemv_nt<3, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 4: return launch_gemv_nt<4, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 5: return launch_gemv_nt<5, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 6: return launch_gemv_nt<6, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 7: return launch_gemv_nt<7, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 8: return launch_gemv_nt<8, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
     default: return fail(GMLP_ERR_INVALID_ARG, "GEMV path needs 1 <= T <= 8 (T=%d)", s.N);
     }
 }
 
-
+// The gate/up step: H = bf16(act(r G) * (r U)).  With RMSNorm the GEMV
+// kernel computes r itself; the MFMA path computes r for every row first.
 int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, void *H, uint8_t *ws,
-                const Layout &l, hipStream_t st)
+                const Layout &l, const Variant &v, hipStream_t st)
 {
+    const float *rrms = nullptr;
+    if (v.rms && s.kind != K_GEMV) {
+        float *r = reinterpret_cast<float *>(ws + l.rrms_off);
+        const int per = kRowRmsThreads / 64;
+        hipLaunchKernelGGL(row_rms_kernel, dim3((unsigned)cdiv(s.N, per)), dim3(kRowRmsThreads), 0, st,
+                           static_cast<const uint16_t *>(X), r, s.N, s.K, v.eps);
+        int rc = hip_check(hipGetLastError(), "row RMS launch");
+        if (rc)
+            return rc;
+        rrms = r;
+    }
     switch (s.kind) {
-    case K_GEMM_GU_L: return launch_gemm<GateUpLarge, EPI_SILU_MUL, false>(s, Wg, Wu, X, H, ws, l, st);
-    case K_GEMM_GU_S: return launch_gemm<GateUpSmall, EPI_SILU_MUL, true>(s, Wg, Wu, X, H, ws, l, st);
-    case K_GEMV: return launch_gemv<2, EPI_SILU_MUL>(s, Wg, Wu, X, H, ws, l, st);
+    case K_GEMM_GU_L:
+        return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, st);
+    case K_GEMM_GU_S:
+        return launch_gemm<GateUpSmall, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, rrms, st);
+    case K_GEMV:
+        return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
+                     : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);
     default: return fail(GMLP_ERR_INVALID_ARG, "no gate/up kernel for this plan");
     }
 }
@@ -371,12 +407,32 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
 int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws, const Layout &l,
              hipStream_t st)
 {
+    const Variant plain;
     switch (s.kind) {
-    case K_GEMM_DN_L: return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, st);
-    case K_GEMM_DN_S: return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, st);
-    case K_GEMV: return launch_gemv<1, EPI_STORE>(s, Wd, nullptr, H, Y, ws, l, st);
+    case K_GEMM_DN_L:
+        return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, st);
+    case K_GEMM_DN_S:
+        return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, st);
+    case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st);
     default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
     }
+}
+
+int check_variant(int activation, float beta, int rmsnorm, float eps, Variant *v)
+{
+    if (activation != GMLP_ACT_SILU && activation != GMLP_ACT_SWISH && activation != GMLP_ACT_SIGMOID)
+        return fail(GMLP_ERR_INVALID_ARG, "unknown activation %d", activation);
+    if (!std::isfinite(beta))
+        return fail(GMLP_ERR_INVALID_ARG, "beta must be finite");
+    if (rmsnorm != 0 && rmsnorm != 1)
+        return fail(GMLP_ERR_INVALID_ARG, "rmsnorm must be 0 or 1 (got %d)", rmsnorm);
+    if (rmsnorm && !(std::isfinite(eps) && eps >= 0.0f))
+        return fail(GMLP_ERR_INVALID_ARG, "eps must be finite and >= 0");
+    v->act = activation;
+    v->beta = activation == GMLP_ACT_SWISH ? beta : 1.0f;
+    v->rms = rmsnorm != 0;
+    v->eps = rmsnorm ? eps : 0.0f;
+    return GMLP_OK;
 }
 
 int check_path(int path, int64_t T)
@@ -441,7 +497,7 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false>";
     case K_GEMM_DN_S: return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true>";
     case K_GEMV:
-        return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0>" : ", 1, 1>");
+        return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
     default: return "none";
     }
 }
@@ -516,11 +572,14 @@ int gmlp_workspace_init(void *workspace, size_t bytes, void *stream)
     return rc ? rc : ok();
 }
 
-int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
-                    int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
+                         int64_t D, int64_t F, int activation, float beta, int rmsnorm, float eps,
+                         int path, void *workspace, size_t ws_bytes, void *stream)
 {
     int rc;
-    if ((rc = validate(T, D, F, X, Wg, Wu, Wd, Y)) || (rc = check_path(path, T)))
+    Variant v;
+    if ((rc = validate(T, D, F, X, Wg, Wu, Wd, Y)) || (rc = check_path(path, T)) ||
+        (rc = check_variant(activation, beta, rmsnorm, eps, &v)))
         return rc;
     if (T == 0)
         return ok();
@@ -531,10 +590,17 @@ int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *W
     uint8_t *ws = static_cast<uint8_t *>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
     void *H = ws + l.h_off;
-    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, ws, l, st)) ||
+    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, ws, l, v, st)) ||
         (rc = run_down(plan.down, H, Wd, Y, ws, l, st)))
         return rc;
     return ok();
+}
+
+int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
+                    int64_t D, int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+{
+    return gmlp_forward_variant(X, Wg, Wu, Wd, Y, T, D, F, GMLP_ACT_SILU, 1.0f, 0, 0.0f, path, workspace,
+                                ws_bytes, stream);
 }
 
 int gmlp_forward_ws(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
@@ -588,11 +654,14 @@ int check_down_args(const void *H, const void *Wd, const void *Y, int64_t T, int
 
 } // namespace
 
-int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
-                    int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
+                         int64_t F, int activation, float beta, int rmsnorm, float eps, int path,
+                         void *workspace, size_t ws_bytes, void *stream)
 {
     int rc;
-    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)) || (rc = check_path(path, T)))
+    Variant v;
+    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)) || (rc = check_path(path, T)) ||
+        (rc = check_variant(activation, beta, rmsnorm, eps, &v)))
         return rc;
     if (T == 0)
         return ok();
@@ -600,10 +669,17 @@ int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int6
     if ((rc = check_workspace(workspace, ws_bytes, l)))
         return rc;
     const Plan plan = make_plan(T, D, F, path);
-    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(workspace), l,
+    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(workspace), l, v,
                           static_cast<hipStream_t>(stream))))
         return rc;
     return ok();
+}
+
+int gmlp_gate_up_ws(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
+                    int64_t F, int path, void *workspace, size_t ws_bytes, void *stream)
+{
+    return gmlp_gate_up_variant(X, Wg, Wu, H, T, D, F, GMLP_ACT_SILU, 1.0f, 0, 0.0f, path, workspace,
+                                ws_bytes, stream);
 }
 
 int gmlp_down_ws(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int64_t D, int path,

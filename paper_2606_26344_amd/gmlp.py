@@ -4,9 +4,13 @@ Argument marshalling only: every step of the Gated MLP runs in the library's
 HIP kernels.  PyTorch supplies device memory and the current HIP stream.  The
 names mirror the C entry points:
 
-    forward(x, wg, wu, wd)   -> gmlp_forward / gmlp_forward_ex
-    gate_up(x, wg, wu)       -> gmlp_gate_up
-    down(h, wd)              -> gmlp_down
+    forward(x, wg, wu, wd)   -> gmlp_forward / gmlp_forward_ex / gmlp_forward_variant
+    gate_up(x, wg, wu)       -> gmlp_gate_up / gmlp_gate_up_ws / gmlp_gate_up_variant
+    down(h, wd)              -> gmlp_down / gmlp_down_ws
+
+forward() and gate_up() also take the members of the Gated MLP family:
+activation "silu" (default), "swish" (g * sigmoid(beta g)) or "sigmoid"
+(GLU), and rmsnorm=True (RMSNorm of X in front, epsilon eps).
 
 Tensors are ``torch.bfloat16``, contiguous, on one HIP device, with shapes
 x [T, D], wg [D, F], wu [D, F], wd [F, D].  Loading fails loudly if the
@@ -27,10 +31,14 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "gmlp.h")
 
 PATH_AUTO, PATH_GEMV, PATH_MFMA = 0, 1, 2
 _PATHS = {"auto": PATH_AUTO, "gemv": PATH_GEMV, "mfma": PATH_MFMA}
+ACT_SILU, ACT_SWISH, ACT_SIGMOID = 0, 1, 2
+ACTIVATIONS = {"silu": ACT_SILU, "swish": ACT_SWISH, "sigmoid": ACT_SIGMOID}
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
 _SZ = ctypes.c_size_t
+_F = ctypes.c_float
+_INT = ctypes.c_int
 
 _SIGNATURES = {
     "gmlp_version": ([], ctypes.c_int),
@@ -44,6 +52,10 @@ _SIGNATURES = {
     "gmlp_forward_ws": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
     "gmlp_forward_ex": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
                         ctypes.c_int),
+    "gmlp_forward_variant": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _INT, _F, _INT, _F, _INT, _P,
+                              _SZ, _P], _INT),
+    "gmlp_gate_up_variant": ([_P, _P, _P, _P, _I64, _I64, _I64, _INT, _F, _INT, _F, _INT, _P, _SZ,
+                              _P], _INT),
     "gmlp_gate_up": ([_P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_down": ([_P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_gate_up_ws": ([_P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
@@ -157,10 +169,18 @@ class Workspace:
         return workspace_size(T, D, F) <= self.nbytes
 
 
+def _variant(activation: str, beta: float, rmsnorm: bool, eps: float):
+    if activation not in ACTIVATIONS:
+        raise ValueError("activation must be one of %s" % sorted(ACTIVATIONS))
+    return ACTIVATIONS[activation], float(beta), int(bool(rmsnorm)), float(eps)
+
+
 def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tensor,
             out: Optional[torch.Tensor] = None, path: str = "auto",
-            workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
-    """Y = (silu(x wg) * (x wu)) wd on the current HIP stream."""
+            workspace: Optional[Workspace] = None, stream=None, activation: str = "silu",
+            beta: float = 1.0, rmsnorm: bool = False, eps: float = 1e-6) -> torch.Tensor:
+    """Y = (act(xn wg) * (xn wu)) wd on the current HIP stream, act = silu by
+    default, xn = x or, with ``rmsnorm``, x / sqrt(mean(x^2) + eps) per row."""
     if x.dim() != 2 or wg.dim() != 2:
         raise ValueError("x and wg must be 2-D")
     T, D = x.shape
@@ -175,20 +195,27 @@ def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tenso
     _expect(out, "out", (T, D), dev)
     lib = library()
     st = _stream(stream)
-    if workspace is None and path == "auto":
+    plain = activation == "silu" and not rmsnorm
+    if workspace is None and path == "auto" and plain:
         _check(lib.gmlp_forward(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F, st))
         return out
     if workspace is None:
         workspace = Workspace(T, D, F, device=dev, stream=stream)
-    _check(lib.gmlp_forward_ex(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
-                               _PATHS[path], _ptr(workspace.buffer), workspace.nbytes, st))
+    if plain:
+        _check(lib.gmlp_forward_ex(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
+                                   _PATHS[path], _ptr(workspace.buffer), workspace.nbytes, st))
+    else:
+        _check(lib.gmlp_forward_variant(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
+                                        *_variant(activation, beta, rmsnorm, eps), _PATHS[path],
+                                        _ptr(workspace.buffer), workspace.nbytes, st))
     return out
 
 
 def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
             out: Optional[torch.Tensor] = None, path: str = "auto",
-            workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
-    """H = bf16(silu(x wg) * (x wu)), H [T, F]."""
+            workspace: Optional[Workspace] = None, stream=None, activation: str = "silu",
+            beta: float = 1.0, rmsnorm: bool = False, eps: float = 1e-6) -> torch.Tensor:
+    """H = bf16(act(xn wg) * (xn wu)), H [T, F] (see forward for the options)."""
     T, D = x.shape
     F = wg.shape[1]
     dev = x.device
@@ -198,15 +225,22 @@ def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
     if out is None:
         out = torch.empty((T, F), dtype=torch.bfloat16, device=dev)
     _expect(out, "out", (T, F), dev)
-    if workspace is None and path == "auto":
+    plain = activation == "silu" and not rmsnorm
+    if workspace is None and path == "auto" and plain:
         _check(library().gmlp_gate_up(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
                                       _stream(stream)))
         return out
     if workspace is None:
         workspace = Workspace(T, D, F, device=dev, stream=stream)
-    _check(library().gmlp_gate_up_ws(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
-                                     _PATHS[path], _ptr(workspace.buffer), workspace.nbytes,
-                                     _stream(stream)))
+    if plain:
+        _check(library().gmlp_gate_up_ws(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
+                                         _PATHS[path], _ptr(workspace.buffer), workspace.nbytes,
+                                         _stream(stream)))
+    else:
+        _check(library().gmlp_gate_up_variant(_ptr(x), _ptr(wg), _ptr(wu), _ptr(out), T, D, F,
+                                              *_variant(activation, beta, rmsnorm, eps),
+                                              _PATHS[path], _ptr(workspace.buffer),
+                                              workspace.nbytes, _stream(stream)))
     return out
 
 

@@ -100,7 +100,8 @@ def test_helpers_validate_too(lib):
 
 def test_describe_names_the_kernels_of_each_path(lib):
     gemv = gmlp.describe(1, 4096, 14336)
-    assert [k[0] for k in gemv] == ["gemv_splitk_kernel<1, 2, 0>", "gemv_splitk_kernel<1, 1, 1>"]
+    assert [k[0] for k in gemv] == ["gemv_splitk_kernel<1, 2, 0, false>",
+                                    "gemv_splitk_kernel<1, 1, 1, false>"]
     for name, grid, block, splits in gemv:
         assert block == 256 and 128 < grid <= 256 and splits > 1
     big = gmlp.describe(4096, 4096, 14336)
@@ -126,3 +127,26 @@ def test_gemv_plan_covers_k_with_at_most_one_round_of_blocks(lib, T, D, F):
         assert grid == strips * splits and block == 256
         assert splits <= K // 8 + 1
         assert grid <= max(512, strips)
+
+
+def test_variant_entry_points_validate_before_launching(lib):
+    n = gmlp.workspace_size(4, 256, 512)
+    base = (A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, 4, 256, 512)
+    fwd = lambda act, beta, rms, eps: lib.gmlp_forward_variant(*base, act, beta, rms, eps, 0,
+                                                                A + 300 * MB, n, None)
+    assert fwd(3, 1.0, 0, 0.0) == 1 and "activation" in gmlp.last_error()
+    assert fwd(-1, 1.0, 0, 0.0) == 1
+    assert fwd(1, float("nan"), 0, 0.0) == 1 and "beta" in gmlp.last_error()
+    assert fwd(1, float("inf"), 0, 0.0) == 1
+    assert fwd(0, 1.0, 2, 0.0) == 1 and "rmsnorm" in gmlp.last_error()
+    assert fwd(0, 1.0, 1, -1e-6) == 1 and "eps" in gmlp.last_error()
+    assert fwd(0, 1.0, 1, float("nan")) == 1
+    gu = lambda act: lib.gmlp_gate_up_variant(A, A + 64 * MB, A + 128 * MB, A + 192 * MB, 4, 256, 512,
+                                              act, 1.0, 0, 0.0, 0, A + 300 * MB, n, None)
+    assert gu(7) == 1
+    # Shape and workspace errors come first, as for gmlp_forward_ex.
+    assert lib.gmlp_forward_variant(A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, 4, 260,
+                                    512, 0, 1.0, 0, 0.0, 0, A + 300 * MB, n, None) == 2
+    assert lib.gmlp_forward_variant(*base, 2, 1.0, 1, 1e-5, 0, A + 300 * MB, n - 256, None) == 4
+    with pytest.raises(ValueError):
+        gmlp._variant("relu", 1.0, False, 0.0)
