@@ -107,6 +107,9 @@ def parse_args(argv=None):
                    help="after the timed region, run plain device copies of %d MiB (a known "
                         "number of bytes) for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE"
                         % (COPY_BYTES >> 20))
+    p.add_argument("--vendor-gemm", action="store_true",
+                   help="also time torch.matmul (the vendor GEMM library) on the same two "
+                        "matmul shapes, for context (X [T,D] x [Wg|Wu] [D,2F], H [T,F] x Wd)")
     p.add_argument("--summarize-profile", metavar="DIR", nargs="+",
                    help="print per-kernel averages from rocprofv3 CSV output directories "
                         "and exit (no GPU work)")
@@ -321,11 +324,48 @@ def run_workload(name, args):
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = COPY_BYTES
         del src, dst
+    if args.vendor_gemm:
+        result["vendor_gemm"] = vendor_gemm(T, D, F, args, wsets[0], x, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds, variant)
     del wsets, x, y, h, ws
     torch.cuda.empty_cache()
     return result
+
+
+def vendor_gemm(T, D, F, args, weights, x, stream):
+    """The vendor library's time for the two matmul shapes of a step (no
+    activation, no fusion): context for the MFMA kernels, not a baseline of
+    the method.  Both weights of the first matmul are concatenated into one
+    [D, 2F] operand, so it is one library call as the fused kernel is one
+    launch."""
+    import torch
+
+    wg, wu, wd = weights
+    w2 = torch.cat([wg, wu], dim=1).contiguous()
+    h = torch.empty((T, F), dtype=torch.bfloat16, device=x.device).normal_()
+
+    def timed(fn, k):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(k):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / k
+
+    gu_ms = timed(lambda: torch.matmul(x, w2), args.steps)
+    dn_ms = timed(lambda: torch.matmul(h, wd), args.steps)
+    out = {"library": "torch.matmul (" + ("hipBLASLt" if torch.version.hip else "vendor") + ")",
+           "gate_up_us": round(gu_ms * 1e3, 3), "down_us": round(dn_ms * 1e3, 3),
+           "gate_up_tflops": round(4.0 * T * D * F / (gu_ms / 1e3) / 1e12, 3),
+           "down_tflops": round(2.0 * T * D * F / (dn_ms / 1e3) / 1e12, 3)}
+    del w2, h
+    return out
 
 
 def _read_counter_csvs(dirs):
