@@ -294,8 +294,8 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if constexpr (RMS) {
             // The whole row's sum of squares, splits added in order; the
-            // loads of 32 / NT splits are in flight at once.
-            constexpr int C = NT >= 32 ? 1 : 32 / NT;
+            // loads of 8 / NT splits are in flight at once.
+            constexpr int C = NT >= 8 ? 1 : 8 / NT;
             float tot[NT];
             for (int s0 = 0; s0 < p.splits; s0 += C) {
                 float x[C][NT];
