@@ -293,63 +293,65 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if constexpr (RMS) {
-            // The whole row's sum of squares, splits added in order; the
-            // loads of 8 / NT splits are in flight at once.
-            constexpr int C = NT >= 8 ? 1 : 8 / NT;
+            // The whole row's sum of squares, splits added in order, with
+            // the same unconditional loads as the column sums.
+            constexpr int C = NT <= 2 ? 4 : 2;
             float tot[NT];
             for (int s0 = 0; s0 < p.splits; s0 += C) {
                 float x[C][NT];
 #pragma unroll
-                for (int u = 0; u < C; ++u)
+                for (int u = 0; u < C; ++u) {
+                    const int sp = s0 + u < p.splits ? s0 + u : split;
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+                        x[u][t] = __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+#pragma unroll
+                for (int u = 0; u < C; ++u) {
+                    const int sp = s0 + u;
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
-                        const int sp = s0 + u;
-                        x[u][t] = sp == split ? ss[t]
-                                  : sp < p.splits ? __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED,
-                                                                      __HIP_MEMORY_SCOPE_AGENT)
-                                                  : 0.0f;
+                        const float xv = sp == split ? ss[t] : x[u][t];
+                        tot[t] = sp == 0 ? xv : sp < p.splits ? tot[t] + xv : tot[t];
                     }
-#pragma unroll
-                for (int u = 0; u < C; ++u)
-                    if (s0 + u < p.splits)
-#pragma unroll
-                        for (int t = 0; t < NT; ++t)
-                            tot[t] = s0 + u == 0 ? x[u][t] : tot[t] + x[u][t];
+                }
             }
 #pragma unroll
             for (int t = 0; t < NT; ++t)
                 ss[t] = tot[t];
         }
         if (mvalid) {
-            // Sum the splits in order 0, 1, 2, ...; the loads of C splits
-            // (about 32 values per thread) are in flight at once.
-            constexpr int C = NW * NT >= 32 ? 1 : 32 / (NW * NT);
+            // Sum the splits in order 0, 1, 2, ...; the loads of C splits are
+            // in flight at once.  They are unconditional (a slot past the
+            // last split reloads this block's own), so there are no
+            // branches; the values past the last split are not added.
+            constexpr int C = NT <= 2 ? 4 : 2;
             const size_t stride = (size_t)NW * NT * M;
             const float *src = &p.partial[m];
             float sum[NW][NT];
             for (int s0 = 0; s0 < p.splits; s0 += C) {
                 float x[C][NW][NT];
 #pragma unroll
-                for (int u = 0; u < C; ++u)
+                for (int u = 0; u < C; ++u) {
+                    const int sp = s0 + u < p.splits ? s0 + u : split;
+#pragma unroll
+                    for (int w = 0; w < NW; ++w)
+#pragma unroll
+                        for (int t = 0; t < NT; ++t)
+                            x[u][w][t] = __hip_atomic_load(src + sp * stride + ((size_t)w * NT + t) * M,
+                                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+#pragma unroll
+                for (int u = 0; u < C; ++u) {
+                    const int sp = s0 + u;
 #pragma unroll
                     for (int w = 0; w < NW; ++w)
 #pragma unroll
                         for (int t = 0; t < NT; ++t) {
-                            const int sp = s0 + u;
-                            x[u][w][t] = sp == split ? v[w][t]
-                                         : sp < p.splits
-                                             ? __hip_atomic_load(src + sp * stride + ((size_t)w * NT + t) * M,
-                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                             : 0.0f;
+                            const float xv = sp == split ? v[w][t] : x[u][w][t];
+                            sum[w][t] = sp == 0 ? xv : sp < p.splits ? sum[w][t] + xv : sum[w][t];
                         }
-#pragma unroll
-                for (int u = 0; u < C; ++u)
-                    if (s0 + u < p.splits)
-#pragma unroll
-                        for (int w = 0; w < NW; ++w)
-#pragma unroll
-                            for (int t = 0; t < NT; ++t)
-                                sum[w][t] = s0 + u == 0 ? x[u][w][t] : sum[w][t] + x[u][w][t];
+                }
             }
 #pragma unroll
             for (int w = 0; w < NW; ++w)
