@@ -62,3 +62,25 @@ def brute_gated_mlp(X, Wg, Wu, Wd, activation="silu", beta=1.0, rmsnorm=False, e
             row.append(acc)
         Y.append(row)
     return Y
+
+
+def brute_softmax_matmul(X, Y):
+    """Z = softmax(X) Y for X [M][K], Y [K][N] as nested lists of floats:
+    exp of every entry, the row sum, the divide, then the matmul (the graph
+    of Fig. fig:softmax-matmul-comp-graph (a), Appendix B)."""
+    M, K, N = len(X), len(Y), len(Y[0])
+    Z = []
+    for i in range(M):
+        e = [math.exp(X[i][k]) for k in range(K)]
+        s = 0.0
+        for v in e:
+            s += v
+        a = [v / s for v in e]
+        row = []
+        for j in range(N):
+            acc = 0.0
+            for k in range(K):
+                acc += a[k] * Y[k][j]
+            row.append(acc)
+        Z.append(row)
+    return Z
