@@ -4,8 +4,8 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--variant silu|swiglu|glu|rmsnorm|rmsnorm_swiglu]
 
-One step is one full pass of the hot path (one fused persistent GEMV kernel
-for T <= 7, else a gate/up kernel and a down kernel) over one batch of
+One step is one full pass of the hot path (a gate/up kernel and a down
+kernel: split-K GEMVs for T <= 8, MFMA GEMMs above) over one batch of
 synthetic inputs already resident in HBM.  W untimed steps,
 then exactly K steps timed with HIP events on the library's stream,
 bracketed by device synchronisation (the paper times 100 runs after 20
@@ -19,16 +19,20 @@ Prints one JSON line per workload (the default workload is the T=1 decode
 shape) with:
   value      whole-job throughput: GB/s of algorithmic bytes 2(3DF + 2TD)
              for memory-bound shapes, TFLOP/s of 6TDF for compute-bound ones;
-  roofline   the dominant kernel timed with HIP events on the library's
-             stream (the fused kernel, which is the whole step, or else the
-             gate/up kernel launched on its own): its algorithmic bytes or
-             flops per launch over its average duration, against the MI355X
-             peak (8 TB/s HBM, 2.5 PFLOP/s dense bf16);
+  roofline   the dominant kernel (the gate/up kernel) launched on its own
+             and timed with HIP events on the library's stream: its
+             algorithmic bytes or flops per launch over its average
+             duration, against the MI355X peak (8 TB/s HBM, 2.5 PFLOP/s
+             dense bf16);
   cpu_baseline  the CPU fp64 oracle on this host's cores, on a bounded
              sample of the same workload, scaled to the same unit.
 --variant selects a member of the Gated MLP family (default: the SiLU Gated
 MLP): swiglu = swish gate with beta 1.702, glu = sigmoid gate, rmsnorm =
 RMSNorm of X in front (eps 1e-6), rmsnorm_swiglu = both.
+--workload softmax_matmul (M = K = N = 8192) or softmax_matmul_tiny benches
+the second workload, Z = softmax(X) Y computed as (exp(X - rowmax) Y) / rowsum
+(one exp/row-sum kernel, then the matmul with the divide in its epilogue):
+value in TFLOP/s of 2MKN, the matmul kernel as the dominant one.
 Only one GPU is used: --gpus above 1 exits with a message.
 """
 from __future__ import annotations
@@ -43,6 +47,7 @@ import time
 
 METRIC = ("Gated-MLP TFLOP/s & % bf16 MFMA peak (prefill); "
           "GB/s & % HBM peak (decode)")
+SMM_METRIC = "Softmax+MatMul TFLOP/s & % bf16 MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published (no sparsity)
 RIDGE = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)  # ~312 FLOP/B
@@ -94,7 +99,8 @@ def parse_args(argv=None):
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="decode",
-                   help="decode | tiny | small_batch | prefill | large_prefill | all")
+                   help="decode | tiny | small_batch | prefill | large_prefill | "
+                        "softmax_matmul | softmax_matmul_tiny | all")
     p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
     p.add_argument("--copies", type=int, default=0,
@@ -333,6 +339,210 @@ def run_workload(name, args):
     return result
 
 
+def smm_algorithmic(M, K, N):
+    """Softmax+MatMul: bytes any method must move (X, Y, Z) and FLOPs (2MKN)."""
+    return 2.0 * (M * K + K * N + M * N), 2.0 * M * K * N
+
+
+def exp_rows_algorithmic(M, K):
+    """Per launch of the exp/row-sum kernel: reads X, writes P and the sums."""
+    return 2.0 * M * K * 2 + 4.0 * M
+
+
+def smm_cpu_baseline(X, Y, bound, budget_s):
+    import numpy as np
+
+    from oracle import softmax_matmul as so
+
+    orc = so.default_oracle()
+    M, K = X.shape
+    N = Y.shape[1]
+    nbytes, flops = smm_algorithmic(M, K, N)
+    threads = orc_threads()
+    t0 = time.perf_counter()
+    orc.rows(X, Y, rows=[0])
+    t_row = max(time.perf_counter() - t0, 1e-6)
+    n = int(max(1, min(M, budget_s // t_row)))
+    rows = np.linspace(0, M - 1, n).round().astype(np.int64) if n < M else None
+    reps = 1 if n < M else int(max(1, min(100000, budget_s // (t_row * M))))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        orc.rows(X, Y, rows=rows)
+    t_total = time.perf_counter() - t0
+    t_full = (t_total / reps) * M / (M if rows is None else n)
+    if bound == "hbm":
+        value, unit = nbytes / t_full / 1e9, "GB/s"
+    else:
+        value, unit = flops / t_full / 1e12, "TFLOP/s"
+    if rows is None:
+        sample = "all %d rows, %d repetitions (%.1f s)" % (M, reps, t_total)
+    else:
+        sample = ("%d of %d rows (evenly spaced), %d repetition(s) in %.1f s, "
+                  "time extrapolated x%.1f to the full step" % (n, M, reps, t_total, M / n))
+    return {"value": round(value, 6), "unit": unit, "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds_per_step": t_full}
+
+
+def orc_threads():
+    import oracle
+
+    return oracle.default_oracle().max_threads()
+
+
+def run_softmax_matmul(name, args):
+    import torch
+
+    from paper_2606_26344_amd import gmlp
+    from paper_2606_26344_amd import inputs as I
+    from paper_2606_26344_amd import softmax_matmul as smm
+
+    w = I.SOFTMAX_MATMUL_WORKLOADS[name]
+    M, K, N = w.M, w.K, w.N
+    nbytes, flops = smm_algorithmic(M, K, N)
+    bound = "hbm" if flops / nbytes < RIDGE else "mfma"
+    lib = gmlp.library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    X, Y = I.generate_softmax_matmul(M, K, N, seed=w.seed, logit_scale=w.logit_scale)
+    t_gen = time.perf_counter() - t_gen
+    x, y = gmlp.from_bf16_bits(X, dev), gmlp.from_bf16_bits(Y, dev)
+    z = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    p = torch.empty((M, K), dtype=torch.bfloat16, device=dev)
+    sums = torch.empty((M,), dtype=torch.float32, device=dev)
+    ws = smm.make_workspace(M, K, N, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    P = ctypes.c_void_p
+    xp, yp, zp, pp, sp = (P(t.data_ptr()) for t in (x, y, z, p, sums))
+    wsp = P(ws.buffer.data_ptr())
+    auto = gmlp.PATH_AUTO
+
+    def step(i):
+        return lib.softmax_matmul_ws(xp, yp, zp, M, K, N, auto, wsp, ws.nbytes, st)
+
+    def exp_rows_only(i):
+        return lib.softmax_matmul_exp_rows(xp, pp, sp, M, K, st)
+
+    def divide_only(i):
+        return lib.softmax_matmul_divide_ws(pp, sp, yp, zp, M, K, N, auto, wsp, ws.nbytes, st)
+
+    def timed(fn, k):
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for i in range(k):
+            rc = fn(i)
+            if rc:
+                raise gmlp.GmlpError(rc, gmlp.last_error())
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / k
+
+    for i in range(args.warmup):
+        if step(i):
+            raise gmlp.GmlpError(1, gmlp.last_error())
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ms_per_step = timed(step, args.steps)
+    wall = time.perf_counter() - wall0
+    k_kernel = max(args.steps, 20)
+    exp_ms = timed(exp_rows_only, k_kernel)
+    mm_ms = timed(divide_only, k_kernel)
+    plan = smm.describe(M, K, N)
+
+    sec = ms_per_step / 1e3
+    if bound == "hbm":
+        value, unit = nbytes / sec / 1e9, "GB/s"
+    else:
+        value, unit = flops / sec / 1e12, "TFLOP/s"
+    dom_kernel = plan[1][0]
+    if bound == "hbm":
+        dom = 2.0 * (M * K + K * N + M * N) + 4.0 * M
+        achieved, peak, r_unit = dom / (mm_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+        per_launch = "%.4g bytes" % dom
+    else:
+        achieved, peak, r_unit = flops / (mm_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+        per_launch = "%.4g flop" % flops
+    exp_bytes = exp_rows_algorithmic(M, K)
+    props = torch.cuda.get_device_properties(dev)
+    result = {
+        "metric": SMM_METRIC,
+        "value": round(value, 3),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: M=%d, K=%d, N=%d, logits N(0, %g^2)" % (name, M, K, N, w.logit_scale),
+            "M": M, "K": K, "N": N,
+            "path": "gemv" if M <= 8 else "mfma",
+            "kernels": [{"name": k, "grid": g, "block": b, "k_splits": s_} for k, g, b, s_ in plan],
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": bound,
+            "achieved": round(achieved, 3),
+            "peak": peak,
+            "unit": r_unit,
+            "frac": round(achieved / peak, 4),
+            "traffic": committed_traffic(name, dom_kernel),
+            "kernel": dom_kernel,
+            "per_launch": per_launch,
+            "avg_launch_us": round(mm_ms * 1e3, 3),
+        },
+        "step": {
+            "gbs": round(nbytes / sec / 1e9, 3),
+            "tflops": round(flops / sec / 1e12, 3),
+            "frac_bf16_peak": round(flops / sec / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "exp_rows_alone_us": round(exp_ms * 1e3, 3),
+            "exp_rows_gbs": round(exp_bytes / (exp_ms / 1e3) / 1e9, 3),
+            "exp_rows_frac_hbm_peak": round(exp_bytes / (exp_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+            "exp_rows_traffic": committed_traffic(name, plan[0][0]),
+            "matmul_divide_alone_us": round(mm_ms * 1e3, 3),
+            "wall_s": round(wall, 4),
+        },
+        "device": {"name": props.name, "cus": props.multi_processor_count,
+                   "arch": getattr(props, "gcnArchName", "")},
+        "input_generation_s": round(t_gen, 2),
+    }
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1, out=dst)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = COPY_BYTES
+        del src, dst
+    if args.vendor_gemm:
+        # Context: the vendor library's plain matmul on the same shape (no
+        # softmax, no divide), and torch's softmax followed by it.
+        a = torch.randn((M, K), device=dev).to(torch.bfloat16)
+        plain = lambda i: torch.matmul(a, y, out=z) is None  # noqa: E731
+        composed = lambda i: torch.matmul(torch.softmax(x, dim=1), y, out=z) is None  # noqa: E731
+        for i in range(args.warmup):
+            plain(i)
+            composed(i)
+        tm = timed(plain, k_kernel)
+        ts = timed(composed, k_kernel)
+        result["vendor_gemm"] = {"matmul_us": round(tm * 1e3, 3),
+                                 "matmul_tflops": round(flops / (tm / 1e3) / 1e12, 3),
+                                 "softmax_then_matmul_us": round(ts * 1e3, 3)}
+        del a
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = smm_cpu_baseline(X, Y, bound, args.cpu_seconds)
+    del x, y, z, p, sums, ws
+    torch.cuda.empty_cache()
+    return result
+
+
 def vendor_gemm(T, D, F, args, weights, x, stream):
     """The vendor library's time for the two matmul shapes of a step (no
     activation, no fusion): context for the MFMA kernels, not a baseline of
@@ -447,13 +657,15 @@ def main(argv=None):
         return 2
     from paper_2606_26344_amd import inputs as I
 
-    names = list(I.WORKLOADS) if args.workload == "all" else [args.workload]
+    names = (list(I.WORKLOADS) + list(I.SOFTMAX_MATMUL_WORKLOADS) if args.workload == "all"
+             else [args.workload])
     for name in names:
-        if name not in I.WORKLOADS:
+        if name not in I.WORKLOADS and name not in I.SOFTMAX_MATMUL_WORKLOADS:
             print("unknown workload %r" % name, file=sys.stderr)
             return 2
     for name in names:
-        print(json.dumps(run_workload(name, args)), flush=True)
+        run = run_softmax_matmul if name in I.SOFTMAX_MATMUL_WORKLOADS else run_workload
+        print(json.dumps(run(name, args)), flush=True)
     return 0
 
 

@@ -66,6 +66,9 @@ struct GemmParams {
     int activation;
     float beta;
     const float *rrms;
+    // Store epilogue: per-token divisors [N] (nullptr: none).  Softmax+MatMul
+    // divides its result rows by the softmax sums here.
+    const float *rowdiv;
 };
 
 template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_, int BK_>
@@ -471,7 +474,7 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                             acc[w][mi][ni][4 * j + e] = sum[((w * TM + mi) * TN + ni) * 4 + j][e];
     }
 
-    // ---- epilogue: fp32 -> act(r G) * (r U) -> bf16, 8-byte row-major stores --
+    // ---- epilogue: fp32 -> act(r G) * (r U), or acc / d -> bf16, 8-byte row-major stores --
     float rs[TN];
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) {
@@ -479,6 +482,13 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         rs[ni] = EPI == EPI_GATE_MUL && p.rrms && t < N ? p.rrms[t] : 1.0f;
     }
     const bool scaled = EPI == EPI_GATE_MUL && p.rrms;
+    float ds[TN];
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+        ds[ni] = EPI == EPI_STORE && p.rowdiv && t < N ? p.rowdiv[t] : 1.0f;
+    }
+    const bool divided = EPI == EPI_STORE && p.rowdiv;
 #pragma unroll
     for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
@@ -500,6 +510,8 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                             v[e] = gate_act(g, p.activation, p.beta) * u;
                         } else {
                             v[e] = acc[0][mi][ni][4 * j + e];
+                            if (divided)
+                                v[e] = v[e] / ds[ni];
                         }
                     }
                     u32x2 packed = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};

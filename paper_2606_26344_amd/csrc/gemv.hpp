@@ -48,6 +48,9 @@ struct GemvParams {
     // squares of the activations [splits][NT] fp32 when splits > 1.
     float eps;
     float *ssq;
+    // Store kernel: per-token divisors [NT] (nullptr: none), the softmax sums
+    // of Softmax+MatMul.
+    const float *rowdiv;
 };
 
 constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
@@ -375,6 +378,8 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                 y = gate_act(g, p.activation, p.beta) * u;
             } else {
                 y = v[0][t];
+                if (p.rowdiv)
+                    y = y / p.rowdiv[t];
             }
             p.out[(size_t)t * M + m] = __builtin_bit_cast(uint16_t, (__bf16)y);
         }

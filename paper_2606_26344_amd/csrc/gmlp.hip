@@ -1,10 +1,11 @@
-// libgmlp.so: the C ABI of include/gmlp.h on top of the gfx950 kernels.
+// libgmlp.so: the C ABI of include/gmlp.h (the Gated MLP family) and
+// include/softmax_matmul.h (Softmax+MatMul) on top of the gfx950 kernels.
 //
 // Host side only: argument validation, the choice of kernels and tile
 // configuration for a shape (the library's static analogue of the paper's
 // empirical per-shape selection, Section 4.6), workspace layout and launches.
-// Every arithmetic step of the Gated MLP runs in the kernels of
-// gemm_mfma.hpp, gemv.hpp and rmsnorm.hpp.
+// Every arithmetic step runs in the kernels of gemm_mfma.hpp, gemv.hpp,
+// rmsnorm.hpp and softmax.hpp.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -15,9 +16,11 @@
 #include <string>
 
 #include "gmlp.h"
+#include "softmax_matmul.h"
 #include "gemm_mfma.hpp"
 #include "gemv.hpp"
 #include "rmsnorm.hpp"
+#include "softmax.hpp"
 
 using namespace gmlp;
 
@@ -301,7 +304,8 @@ int hip_check(hipError_t e, const char *what)
 
 template <class S, int EPI, bool SPLIT>
 int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, hipStream_t stream)
+                uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, const float *rowdiv,
+                hipStream_t stream)
 {
     GemmParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -321,6 +325,7 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.activation = v.act;
     p.beta = v.beta;
     p.rrms = rrms;
+    p.rowdiv = rowdiv;
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
     if (s.partial_bytes > (size_t)kNumRecords)
@@ -331,7 +336,7 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
 }
 
 GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                       uint8_t *ws, const Layout &l, const Variant &v)
+                       uint8_t *ws, const Layout &l, const Variant &v, const float *rowdiv)
 {
     GemvParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -351,14 +356,15 @@ GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void
     p.eps = v.eps;
     // Sums of squares follow the column sums of every split.
     p.ssq = p.partial + (size_t)s.splits * 2 * s.N * s.M;
+    p.rowdiv = rowdiv;
     return p;
 }
 
 template <int NT, int NW, int EPI, bool RMS>
 int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                   uint8_t *ws, const Layout &l, const Variant &v, hipStream_t stream)
+                   uint8_t *ws, const Layout &l, const Variant &v, const float *rowdiv, hipStream_t stream)
 {
-    const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l, v);
+    const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l, v, rowdiv);
     hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI, RMS>), dim3(s.blocks), dim3(kGemvThreads), 0,
                        stream, p);
     return hip_check(hipGetLastError(), "GEMV launch");
@@ -366,17 +372,18 @@ int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *ac
 
 template <int NW, int EPI, bool RMS>
 int launch_gemv(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                uint8_t *ws, const Layout &l, const Variant &v, hipStream_t stream)
+                uint8_t *ws, const Layout &l, const Variant &v, hipStream_t stream,
+                const float *rowdiv = nullptr)
 {
     switch (s.N) {
-    case 1: return launch_gemv_nt<1, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 2: return launch_gemv_nt<2, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 3: return launch_gemv_nt<3, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 4: return launch_gemv_nt<4, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 5: return launch_gemv_nt<5, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 6: return launch_gemv_nt<6, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 7: return launch_gemv_nt<7, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
-    case 8: return launch_gemv_nt<8, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, stream);
+    case 1: return launch_gemv_nt<1, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 2: return launch_gemv_nt<2, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 3: return launch_gemv_nt<3, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 4: return launch_gemv_nt<4, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 5: return launch_gemv_nt<5, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 6: return launch_gemv_nt<6, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 7: return launch_gemv_nt<7, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
+    case 8: return launch_gemv_nt<8, NW, EPI, RMS>(s, w0, w1, act, out, ws, l, v, rowdiv, stream);
     default: return fail(GMLP_ERR_INVALID_ARG, "GEMV path needs 1 <= T <= 8 (T=%d)", s.N);
     }
 }
@@ -399,9 +406,9 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     }
     switch (s.kind) {
     case K_GEMM_GU_L:
-        return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, st);
+        return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_S:
-        return launch_gemm<GateUpSmall, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, rrms, st);
+        return launch_gemm<GateUpSmall, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);
@@ -409,16 +416,20 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     }
 }
 
+// The down step, Y = bf16(H Wd), or with row divisors d, Y = bf16((H Wd) / d)
+// row by row (the divide of Softmax+MatMul moved past its matmul).
 int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws, const Layout &l,
-             hipStream_t st)
+             hipStream_t st, const float *rowdiv = nullptr)
 {
     const Variant plain;
     switch (s.kind) {
     case K_GEMM_DN_L:
-        return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, st);
+        return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
+                                                         st);
     case K_GEMM_DN_S:
-        return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, st);
-    case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st);
+        return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
+                                                        st);
+    case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);
     default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
     }
 }
@@ -629,6 +640,8 @@ int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, 
     return gmlp_forward_ex(X, Wg, Wu, Wd, Y, T, D, F, GMLP_PATH_AUTO, s.ptr, l.total, stream);
 }
 
+} // extern "C"
+
 namespace {
 
 int check_gate_up_args(const void *X, const void *Wg, const void *Wu, const void *H, int64_t T,
@@ -658,6 +671,8 @@ int check_down_args(const void *H, const void *Wd, const void *Y, int64_t T, int
 }
 
 } // namespace
+
+extern "C" {
 
 int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
                          int64_t F, int activation, float beta, int rmsnorm, float eps, int path,
@@ -732,6 +747,199 @@ int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int6
     if ((rc = s.alloc(l.total, l, static_cast<hipStream_t>(stream))))
         return rc;
     return gmlp_down_ws(H, Wd, Y, T, F, D, GMLP_PATH_AUTO, s.ptr, l.total, stream);
+}
+
+} // extern "C"
+
+// ---- Softmax+MatMul --------------------------------------------------------------
+// Z = softmax(X) Y computed as (P Y) / s: softmax_exp_rows_kernel writes
+// P = exp(X - rowmax) and the row sums s, then the Gated MLP's down-step
+// kernels (T = M tokens, F = K contracted rows, D = N output columns) run the
+// matmul with s as the row divisors of their epilogue.
+
+namespace {
+
+int check_smm_shape(int64_t M, int64_t K, int64_t N)
+{
+    if (M < 0 || K <= 0 || N <= 0)
+        return fail(GMLP_ERR_INVALID_ARG, "invalid shape M=%lld K=%lld N=%lld (need M >= 0, K > 0, N > 0)",
+                    (long long)M, (long long)K, (long long)N);
+    if (K % 8 || N % 8)
+        return fail(GMLP_ERR_UNSUPPORTED, "K=%lld and N=%lld must be multiples of 8", (long long)K,
+                    (long long)N);
+    if (K > kMaxDim || N > kMaxDim || M > kMaxTokens)
+        return fail(GMLP_ERR_UNSUPPORTED, "shape M=%lld K=%lld N=%lld exceeds the supported range "
+                    "(K, N <= %lld, M <= %lld)", (long long)M, (long long)K, (long long)N,
+                    (long long)kMaxDim, (long long)kMaxTokens);
+    return GMLP_OK;
+}
+
+int check_smm_args(const void *X, const void *Y, const void *Z, int64_t M, int64_t K, int64_t N)
+{
+    int rc;
+    if ((rc = check_smm_shape(M, K, N)))
+        return rc;
+    if ((rc = check_ptr(X, "X", M > 0)) || (rc = check_ptr(Y, "Y", true)) || (rc = check_ptr(Z, "Z", M > 0)))
+        return rc;
+    const size_t xb = (size_t)M * K * 2, yb = (size_t)K * N * 2, zb = (size_t)M * N * 2;
+    if (overlaps(Z, zb, X, xb) || overlaps(Z, zb, Y, yb))
+        return fail(GMLP_ERR_INVALID_ARG, "Z overlaps an input");
+    return GMLP_OK;
+}
+
+Step smm_matmul_step(int64_t M, int64_t K, int64_t N, int path) { return make_plan(M, N, K, path).down; }
+
+// Counter block, then P [M, K] bf16 (in the H slot), the matmul's split-K
+// partial sums, and the row sums [M] fp32 (in the row-scale slot).  Sized for
+// every path of the shape.
+Layout smm_layout(int64_t M, int64_t K, int64_t N)
+{
+    int counters = 0;
+    size_t partial = 0;
+    for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {
+        if (path == GMLP_PATH_GEMV && M > kGemvMaxTokens)
+            continue;
+        const Step s = smm_matmul_step(M, K, N, path);
+        counters = std::max(counters, s.counters);
+        partial = std::max(partial, s.partial_bytes);
+    }
+    Layout l;
+    l.counters_off = 0;
+    l.counters = counters;
+    l.h_off = kCounterBytes;
+    l.partial_off = l.h_off + align_up((size_t)M * K * 2);
+    l.rrms_off = l.partial_off + align_up(partial);
+    l.total = l.rrms_off + align_up((size_t)M * sizeof(float));
+    return l;
+}
+
+int launch_softmax_rows(const void *X, uint16_t *P, float *sums, int64_t M, int64_t K, hipStream_t st)
+{
+    const dim3 grid((unsigned)cdiv(M, kSoftmaxThreads / 64)), block(kSoftmaxThreads);
+    const uint16_t *x = static_cast<const uint16_t *>(X);
+    switch (softmax_chunks_per_lane((int)K)) {
+    case 1: hipLaunchKernelGGL(softmax_exp_rows_kernel<1>, grid, block, 0, st, x, P, sums, (int)M, (int)K); break;
+    case 2: hipLaunchKernelGGL(softmax_exp_rows_kernel<2>, grid, block, 0, st, x, P, sums, (int)M, (int)K); break;
+    case 4: hipLaunchKernelGGL(softmax_exp_rows_kernel<4>, grid, block, 0, st, x, P, sums, (int)M, (int)K); break;
+    case 8: hipLaunchKernelGGL(softmax_exp_rows_kernel<8>, grid, block, 0, st, x, P, sums, (int)M, (int)K); break;
+    default:
+        hipLaunchKernelGGL(softmax_exp_rows_kernel<kSoftmaxMaxChunks>, grid, block, 0, st, x, P, sums, (int)M,
+                           (int)K);
+        break;
+    }
+    return hip_check(hipGetLastError(), "softmax exp/row-sum launch");
+}
+
+} // namespace
+
+extern "C" {
+
+size_t softmax_matmul_workspace_size(int64_t M, int64_t K, int64_t N)
+{
+    if (check_smm_shape(M, K, N))
+        return 0;
+    return smm_layout(M, K, N).total;
+}
+
+int softmax_matmul_describe(int64_t M, int64_t K, int64_t N, int path, char *buf, size_t bytes)
+{
+    int rc;
+    if (!buf || !bytes)
+        return fail(GMLP_ERR_INVALID_ARG, "describe needs a buffer");
+    buf[0] = '\0';
+    if ((rc = check_smm_shape(M, K, N)))
+        return rc;
+    if ((rc = check_path(path, M)))
+        return rc;
+    if (M == 0)
+        return ok();
+    const Step s = smm_matmul_step(M, K, N, path);
+    const int r = softmax_chunks_per_lane((int)K);
+    snprintf(buf, bytes, "softmax_exp_rows_kernel<%d> grid=%lld block=%d k_splits=1\n%s grid=%d block=%d k_splits=%d\n",
+             r, (long long)cdiv(M, kSoftmaxThreads / 64), kSoftmaxThreads, kernel_name(s, false).c_str(),
+             s.blocks, s.threads, s.splits);
+    return ok();
+}
+
+int softmax_matmul_ws(const void *X, const void *Y, void *Z, int64_t M, int64_t K, int64_t N, int path,
+                      void *workspace, size_t ws_bytes, void *stream)
+{
+    int rc;
+    if ((rc = check_smm_args(X, Y, Z, M, K, N)) || (rc = check_path(path, M)))
+        return rc;
+    if (M == 0)
+        return ok();
+    const Layout l = smm_layout(M, K, N);
+    if ((rc = check_workspace(workspace, ws_bytes, l)))
+        return rc;
+    if (overlaps(Z, (size_t)M * N * 2, workspace, l.total))
+        return fail(GMLP_ERR_INVALID_ARG, "Z overlaps the workspace");
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    uint16_t *P = reinterpret_cast<uint16_t *>(ws + l.h_off);
+    float *sums = reinterpret_cast<float *>(ws + l.rrms_off);
+    const Step s = smm_matmul_step(M, K, N, path);
+    if ((rc = launch_softmax_rows(X, P, sums, M, K, st)) || (rc = run_down(s, P, Y, Z, ws, l, st, sums)))
+        return rc;
+    return ok();
+}
+
+int softmax_matmul_exp_rows(const void *X, void *P, float *s, int64_t M, int64_t K, void *stream)
+{
+    int rc;
+    if ((rc = check_smm_shape(M, K, 8)) || (rc = check_ptr(X, "X", M > 0)) || (rc = check_ptr(P, "P", M > 0)))
+        return rc;
+    if (M > 0 && !s)
+        return fail(GMLP_ERR_INVALID_ARG, "s is NULL");
+    if (reinterpret_cast<uintptr_t>(s) % 4)
+        return fail(GMLP_ERR_UNSUPPORTED, "s (%p) is not 4-byte aligned", (const void *)s);
+    const size_t xb = (size_t)M * K * 2, sb = (size_t)M * sizeof(float);
+    if (overlaps(P, xb, X, xb) || overlaps(s, sb, X, xb) || overlaps(s, sb, P, xb))
+        return fail(GMLP_ERR_INVALID_ARG, "X, P and s must not overlap");
+    if (M == 0)
+        return ok();
+    if ((rc = launch_softmax_rows(X, static_cast<uint16_t *>(P), s, M, K, static_cast<hipStream_t>(stream))))
+        return rc;
+    return ok();
+}
+
+int softmax_matmul_divide_ws(const void *P, const float *s, const void *Y, void *Z, int64_t M, int64_t K,
+                             int64_t N, int path, void *workspace, size_t ws_bytes, void *stream)
+{
+    int rc;
+    if ((rc = check_smm_args(P, Y, Z, M, K, N)) || (rc = check_path(path, M)))
+        return rc;
+    if (M > 0 && !s)
+        return fail(GMLP_ERR_INVALID_ARG, "s is NULL");
+    if (reinterpret_cast<uintptr_t>(s) % 4)
+        return fail(GMLP_ERR_UNSUPPORTED, "s (%p) is not 4-byte aligned", (const void *)s);
+    if (overlaps(Z, (size_t)M * N * 2, s, (size_t)M * sizeof(float)))
+        return fail(GMLP_ERR_INVALID_ARG, "Z overlaps s");
+    if (M == 0)
+        return ok();
+    const Layout l = smm_layout(M, K, N);
+    if ((rc = check_workspace(workspace, ws_bytes, l)))
+        return rc;
+    if (overlaps(Z, (size_t)M * N * 2, workspace, l.total))
+        return fail(GMLP_ERR_INVALID_ARG, "Z overlaps the workspace");
+    const Step st = smm_matmul_step(M, K, N, path);
+    if ((rc = run_down(st, P, Y, Z, static_cast<uint8_t *>(workspace), l, static_cast<hipStream_t>(stream), s)))
+        return rc;
+    return ok();
+}
+
+int softmax_matmul(const void *X, const void *Y, void *Z, int64_t M, int64_t K, int64_t N, void *stream)
+{
+    int rc;
+    if ((rc = check_smm_args(X, Y, Z, M, K, N)))
+        return rc;
+    if (M == 0)
+        return ok();
+    const Layout l = smm_layout(M, K, N);
+    Scratch s;
+    if ((rc = s.alloc(l.total, l, static_cast<hipStream_t>(stream))))
+        return rc;
+    return softmax_matmul_ws(X, Y, Z, M, K, N, GMLP_PATH_AUTO, s.ptr, l.total, stream);
 }
 
 } // extern "C"

@@ -1,4 +1,6 @@
-"""Python binding of libgmlp.so (the C ABI declared in include/gmlp.h).
+"""Python binding of libgmlp.so (the C ABI declared in include/gmlp.h; the
+Softmax+MatMul entry points of include/softmax_matmul.h are bound in
+``softmax_matmul.py`` on the same library).
 
 Argument marshalling only: every step of the Gated MLP runs in the library's
 HIP kernels.  PyTorch supplies device memory and the current HIP stream.  The
@@ -28,6 +30,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIBRARY = os.path.join(HERE, "libgmlp.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "gmlp.h")
+HEADERS = [HEADER, os.path.join(os.path.dirname(HERE), "include", "softmax_matmul.h")]
 
 PATH_AUTO, PATH_GEMV, PATH_MFMA = 0, 1, 2
 _PATHS = {"auto": PATH_AUTO, "gemv": PATH_GEMV, "mfma": PATH_MFMA}
@@ -61,6 +64,12 @@ _SIGNATURES = {
     "gmlp_gate_up_ws": ([_P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
                         ctypes.c_int),
     "gmlp_down_ws": ([_P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P], ctypes.c_int),
+    "softmax_matmul_workspace_size": ([_I64, _I64, _I64], _SZ),
+    "softmax_matmul_describe": ([_I64, _I64, _I64, _INT, ctypes.c_char_p, _SZ], _INT),
+    "softmax_matmul_ws": ([_P, _P, _P, _I64, _I64, _I64, _INT, _P, _SZ, _P], _INT),
+    "softmax_matmul": ([_P, _P, _P, _I64, _I64, _I64, _P], _INT),
+    "softmax_matmul_exp_rows": ([_P, _P, _P, _I64, _I64, _P], _INT),
+    "softmax_matmul_divide_ws": ([_P, _P, _P, _P, _I64, _I64, _I64, _INT, _P, _SZ, _P], _INT),
 }
 
 _lib = None
@@ -88,10 +97,13 @@ def library() -> ctypes.CDLL:
 
 
 def header_functions() -> list:
-    """Names of the functions include/gmlp.h declares."""
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(gmlp_[a-z_0-9]+)\s*\(", text)))
+    """Names of the functions include/gmlp.h and include/softmax_matmul.h
+    declare."""
+    names = set()
+    for path in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
+        names.update(re.findall(r"\b((?:gmlp|softmax_matmul)(?:_[a-z_0-9]+)?)\s*\(", text))
+    return sorted(names)
 
 
 def version() -> int:
@@ -139,6 +151,10 @@ def describe(T: int, D: int, F: int, path: str = "auto") -> list:
     (name, grid, block, k_splits), in launch order."""
     buf = ctypes.create_string_buffer(1024)
     _check(library().gmlp_describe(T, D, F, _PATHS[path], buf, len(buf)))
+    return _parse_plan(buf)
+
+
+def _parse_plan(buf) -> list:
     out = []
     for line in buf.value.decode().splitlines():
         name, rest = line.rsplit(" grid=", 1)
@@ -152,10 +168,11 @@ def workspace_size(T: int, D: int, F: int) -> int:
 
 
 class Workspace:
-    """A caller-owned workspace for forward(), zeroed once at creation."""
+    """A caller-owned workspace for forward(), zeroed once at creation
+    (``nbytes`` overrides the size gmlp_workspace_size gives)."""
 
-    def __init__(self, T: int, D: int, F: int, device=None, stream=None):
-        n = workspace_size(T, D, F)
+    def __init__(self, T: int, D: int, F: int, device=None, stream=None, nbytes: int = 0):
+        n = nbytes or workspace_size(T, D, F)
         if n == 0:
             raise ValueError("invalid shape T=%d D=%d F=%d" % (T, D, F))
         # 256 bytes of slack so the buffer can be 256-byte aligned.

@@ -1,4 +1,4 @@
-"""Seeded synthetic inputs for the SiLU Gated MLP workloads.
+"""Seeded synthetic inputs for the SiLU Gated MLP and Softmax+MatMul workloads.
 
 This module only draws and encodes inputs; it holds none of the Gated MLP's
 arithmetic, so that the HIP path and the CPU oracle can both be fed the same
@@ -15,6 +15,10 @@ depends only on tensor shapes, Section 6.1):
   * every value rounded once to bf16, round-to-nearest-even.
 Arrays are returned as ``uint16`` bf16 bit patterns, row-major:
 X [T, D], Wg [D, F], Wu [D, F], Wd [F, D].
+
+Softmax+MatMul (Z = softmax(X) Y): the same generator, drawn in the order
+X, Y; logits X ~ N(0, s^2) with s = ``logit_scale`` (1 by default), Y ~ N(0, 1);
+X [M, K], Y [K, N].
 """
 from __future__ import annotations
 
@@ -50,6 +54,31 @@ WORKLOADS: Dict[str, Workload] = {
                              "X rows at unit RMS"),
         Workload("large_prefill", 2048, 8192, 28672,
                  description="large-model prefill: T=2048, D=8192, F=28672"),
+    )
+}
+
+
+@dataclass(frozen=True)
+class SoftmaxMatmulWorkload:
+    name: str
+    M: int
+    K: int
+    N: int
+    logit_scale: float = 1.0
+    seed: int = 0
+    description: str = ""
+
+
+# The paper sweeps every dimension of Softmax+MatMul over 2K, 4K and 8K
+# (table tab:multi-op-eval, Section 6.3); the largest point is the benchmark
+# shape, the tiny one is for full checks against the oracle.
+SOFTMAX_MATMUL_WORKLOADS: Dict[str, SoftmaxMatmulWorkload] = {
+    w.name: w
+    for w in (
+        SoftmaxMatmulWorkload("softmax_matmul_tiny", 16, 256, 512,
+                              description="Softmax+MatMul: M=16, K=256, N=512"),
+        SoftmaxMatmulWorkload("softmax_matmul", 8192, 8192, 8192,
+                              description="Softmax+MatMul: M=8192, K=8192, N=8192"),
     )
 }
 
@@ -130,6 +159,16 @@ def generate(T: int, D: int, F: int, seed: int = 0, unit_rms_rows: bool = False)
     Wu = _draw_bf16(rng, D, F, 1.0 / math.sqrt(D), scratch=scratch)
     Wd = _draw_bf16(rng, F, D, 1.0 / math.sqrt(F), scratch=scratch)
     return X, Wg, Wu, Wd
+
+
+def generate_softmax_matmul(M: int, K: int, N: int, seed: int = 0, logit_scale: float = 1.0):
+    """Draw X [M, K] (logits, N(0, logit_scale^2)) and Y [K, N] (N(0, 1)) as
+    bf16 bit patterns for one Softmax+MatMul problem."""
+    rng = np.random.default_rng(seed)
+    scratch = _Scratch()
+    X = _draw_bf16(rng, M, K, logit_scale, scratch=scratch)
+    Y = _draw_bf16(rng, K, N, 1.0, scratch=scratch)
+    return X, Y
 
 
 def generate_workload(name: str, T: int = None, seed: int = None):

@@ -150,3 +150,65 @@ def test_variant_entry_points_validate_before_launching(lib):
     assert lib.gmlp_forward_variant(*base, 2, 1.0, 1, 1e-5, 0, A + 300 * MB, n - 256, None) == 4
     with pytest.raises(ValueError):
         gmlp._variant("relu", 1.0, False, 0.0)
+
+
+# ---- Softmax+MatMul (include/softmax_matmul.h) --------------------------------
+from paper_2606_26344_amd import softmax_matmul as smm  # noqa: E402
+
+
+def test_softmax_matmul_describe_names_the_kernels(lib):
+    big = smm.describe(8192, 8192, 8192)
+    assert big[0] == ("softmax_exp_rows_kernel<16>", 2048, 256, 1)
+    assert big[1][0].startswith("gemm_mfma_kernel<GemmShape<1,") and big[1][0].endswith(", 1, false>")
+    small = smm.describe(3, 4096, 1032)
+    assert small[0] == ("softmax_exp_rows_kernel<8>", 1, 256, 1)
+    assert small[1][0] == "gemv_splitk_kernel<3, 1, 1, false>"
+    assert smm.describe(3, 4096, 1032, "mfma")[1][0].endswith(", 1, true>")
+    # Chunks per lane: the smallest power of two with 512 columns each that
+    # covers K, at most 16 (longer rows are streamed).
+    for K, r in [(8, 1), (512, 1), (520, 2), (1024, 2), (2048, 4), (4104, 16), (8192, 16),
+                 (16392, 16)]:
+        assert smm.describe(1, K, 64)[0][0] == "softmax_exp_rows_kernel<%d>" % r, K
+    assert smm.describe(0, 64, 64) == []
+
+
+def test_softmax_matmul_rejects_bad_arguments(lib):
+    buf = ctypes.create_string_buffer(256)
+    assert lib.softmax_matmul_describe(4, 260, 512, 0, buf, 256) == 2  # K % 8
+    assert lib.softmax_matmul_describe(4, 256, 36, 0, buf, 256) == 2   # N % 8
+    assert lib.softmax_matmul_describe(-1, 256, 512, 0, buf, 256) == 1
+    assert lib.softmax_matmul_describe(9, 256, 512, 1, buf, 256) == 2  # GEMV needs M <= 8
+    assert lib.softmax_matmul_workspace_size(4, 260, 512) == 0
+    assert lib.softmax_matmul_workspace_size(4, 256, 0) == 0
+    n = smm.workspace_size(4, 256, 512)
+    assert n >= 4 * 256 * 2 + 4 * 4
+    X, Y, Z, W = A, A + 64 * MB, A + 128 * MB, A + 192 * MB
+    call = lambda *a: lib.softmax_matmul_ws(*a)
+    assert call(None, Y, Z, 4, 256, 512, 0, W, n, None) == 1
+    assert call(X, Y, None, 4, 256, 512, 0, W, n, None) == 1
+    assert call(X + 8, Y, Z, 4, 256, 512, 0, W, n, None) == 2   # misaligned
+    assert call(X, Y, X, 4, 256, 512, 0, W, n, None) == 1       # Z on X
+    assert call(X, Y, Y + 64, 4, 256, 512, 0, W, n, None) == 1  # Z on Y
+    assert call(X, Y, Z, 4, 256, 512, 0, W, n - 256, None) == 4  # workspace too small
+    assert call(X, Y, Z, 4, 256, 512, 0, W + 16, n, None) == 2  # workspace misaligned
+    assert call(X, Y, Z, 4, 256, 512, 0, None, n, None) == 1
+    assert call(X, Y, W + 256, 4, 256, 512, 0, W, n, None) == 1  # Z inside the workspace
+    assert call(X, Y, Z, 4, 256, 512, 5, W, n, None) == 1        # unknown path
+    assert call(None, Y, None, 0, 256, 512, 0, None, 0, None) == 0  # M == 0: nothing to do
+    assert lib.softmax_matmul(X, Y, X, 4, 256, 512, None) == 1
+
+
+def test_softmax_matmul_halves_validate_before_launching(lib):
+    X, P, S, Y, Z, W = A, A + 64 * MB, A + 128 * MB, A + 160 * MB, A + 192 * MB, A + 256 * MB
+    n = smm.workspace_size(4, 256, 512)
+    assert lib.softmax_matmul_exp_rows(X, P, None, 4, 256, None) == 1
+    assert lib.softmax_matmul_exp_rows(X, P, S + 2, 4, 256, None) == 2
+    assert lib.softmax_matmul_exp_rows(X, X + 512, S, 4, 256, None) == 1  # P on X
+    assert lib.softmax_matmul_exp_rows(X, P, P + 16, 4, 256, None) == 1    # s on P
+    assert lib.softmax_matmul_exp_rows(X, P, S, 4, 260, None) == 2
+    assert lib.softmax_matmul_exp_rows(None, None, None, 0, 256, None) == 0
+    div = lambda *a: lib.softmax_matmul_divide_ws(*a)
+    assert div(P, None, Y, Z, 4, 256, 512, 0, W, n, None) == 1
+    assert div(P, S, Y, S, 4, 256, 512, 0, W, n, None) == 1   # Z on s
+    assert div(P, S, Y, Z, 4, 256, 512, 0, W, n - 256, None) == 4
+    assert div(P, S, Y, Z, 9, 256, 512, 1, W, n, None) == 2   # GEMV needs M <= 8
