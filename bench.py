@@ -144,11 +144,13 @@ def cpu_baseline(w, X, Wg, Wu, Wd, bound, budget_s, variant=None):
     T, D, F = w.T, w.D, w.F
     nbytes, flops = algorithmic(T, D, F)
     threads = orc.max_threads()
-    # Calibrate on one row, then size the sample to fill the time budget.
-    t0 = time.perf_counter()
+    # Calibrate on a few rows (as many as the threads, which work on whole
+    # rows), then size the sample to fill the time budget.
     variant = variant or {}
-    orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=[0], **variant)
-    t_row = max(time.perf_counter() - t0, 1e-6)
+    c = min(T, 2 * threads)
+    t0 = time.perf_counter()
+    orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=np.arange(c), **variant)
+    t_row = max((time.perf_counter() - t0) / c, 1e-6)
     n = int(max(1, min(T, budget_s // t_row)))
     rows = np.linspace(0, T - 1, n).round().astype(np.int64) if n < T else None
     reps = 1 if n < T else int(max(1, min(100000, budget_s // (t_row * T))))
@@ -359,9 +361,10 @@ def smm_cpu_baseline(X, Y, bound, budget_s):
     N = Y.shape[1]
     nbytes, flops = smm_algorithmic(M, K, N)
     threads = orc_threads()
+    c = min(M, 2 * threads)
     t0 = time.perf_counter()
-    orc.rows(X, Y, rows=[0])
-    t_row = max(time.perf_counter() - t0, 1e-6)
+    orc.rows(X, Y, rows=np.arange(c))
+    t_row = max((time.perf_counter() - t0) / c, 1e-6)
     n = int(max(1, min(M, budget_s // t_row)))
     rows = np.linspace(0, M - 1, n).round().astype(np.int64) if n < M else None
     reps = 1 if n < M else int(max(1, min(100000, budget_s // (t_row * M))))
@@ -631,7 +634,7 @@ def summarize_profile(args):
         for k, cs in counters.items():
             if "gmlp::" in k:
                 # The name gmlp_describe gives the kernel.
-                short = k.split("(gmlp::")[0].replace("void ", "", 1).replace("gmlp::", "")
+                short = k.split("(")[0].replace("void ", "", 1).replace("gmlp::", "")
                 fe, wr = cs.get("FETCH_SIZE"), cs.get("WRITE_SIZE")
                 tb = None
                 if fe is not None and wr is not None and f_fetch and f_write:
