@@ -255,6 +255,10 @@ def run_workload(name, args):
     gate_up_ms = timed(gate_up_only, k_kernel)
     down_ms = timed(down_only, k_kernel)
     plan = gmlp.describe(T, D, F)
+    stats = per_step_stats(step, k_kernel, stream)
+    # Context only: every step on the same weight copy, which the 256 MB
+    # Infinity Cache may then serve in part.
+    unrotated_ms = timed(lambda i: step(0), k_kernel) if copies > 1 else None
 
     sec = ms_per_step / 1e3
     if bound == "hbm":
@@ -317,6 +321,8 @@ def run_workload(name, args):
             "gate_up_alone_us": round(gate_up_ms * 1e3, 3),
             "down_alone_us": round(down_ms * 1e3, 3),
             "wall_s": round(wall, 4),
+            "single_steps": stats,
+            "unrotated_weights_us": None if unrotated_ms is None else round(unrotated_ms * 1e3, 3),
         },
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "arch": getattr(props, "gcnArchName", "")},
@@ -339,6 +345,29 @@ def run_workload(name, args):
     del wsets, x, y, h, ws
     torch.cuda.empty_cache()
     return result
+
+
+def per_step_stats(fn, k, stream):
+    """Median, mean and min of k single steps, each between its own pair of
+    HIP events on the library's stream (after the timed region; the value
+    reported is still the K-step bracket)."""
+    import statistics
+
+    import torch
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(k)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        rc = fn(i)
+        if rc:
+            raise RuntimeError("step failed with status %d" % rc)
+        b.record(stream)
+    torch.cuda.synchronize()
+    us = [a.elapsed_time(b) * 1e3 for a, b in evs]
+    return {"median_us": round(statistics.median(us), 3), "mean_us": round(statistics.fmean(us), 3),
+            "min_us": round(min(us), 3), "steps": k}
 
 
 def smm_algorithmic(M, K, N):
@@ -454,6 +483,7 @@ def run_softmax_matmul(name, args):
     exp_ms = timed(exp_rows_only, k_kernel)
     mm_ms = timed(divide_only, k_kernel)
     plan = smm.describe(M, K, N)
+    stats = per_step_stats(step, k_kernel, stream)
 
     sec = ms_per_step / 1e3
     if bound == "hbm":
@@ -511,6 +541,7 @@ def run_softmax_matmul(name, args):
             "exp_rows_traffic": committed_traffic(name, plan[0][0]),
             "matmul_divide_alone_us": round(mm_ms * 1e3, 3),
             "wall_s": round(wall, 4),
+            "single_steps": stats,
         },
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "arch": getattr(props, "gcnArchName", "")},
@@ -589,6 +620,7 @@ def _read_counter_csvs(dirs):
 
     tot = defaultdict(lambda: defaultdict(float))
     disp = defaultdict(lambda: defaultdict(set))
+    span = defaultdict(dict)  # kernel -> dispatch -> duration (ns) in the counter run
     for d in dirs:
         for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             with open(path) as fh:
@@ -596,7 +628,13 @@ def _read_counter_csvs(dirs):
                     k, c = r["Kernel_Name"], r["Counter_Name"]
                     tot[k][c] += float(r["Counter_Value"])
                     disp[k][c].add((path, r["Dispatch_Id"]))
-    return {k: {c: v / len(disp[k][c]) for c, v in cs.items()} for k, cs in tot.items()}
+                    if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+                        span[k][(path, r["Dispatch_Id"])] = (float(r["End_Timestamp"])
+                                                             - float(r["Start_Timestamp"]))
+    out = {k: {c: v / len(disp[k][c]) for c, v in cs.items()} for k, cs in tot.items()}
+    for k, spans in span.items():
+        out[k]["duration_ns"] = sum(spans.values()) / len(spans)
+    return out
 
 
 def _read_kernel_stats(dirs):
@@ -617,6 +655,14 @@ def summarize_profile(args):
         print(k)
         for c, v in sorted(cs.items()):
             print("    %-28s %.6g" % (c, v))
+        if cs.get("GRBM_GUI_ACTIVE") and cs.get("duration_ns", 0) > 100e3:
+            # GRBM_GUI_ACTIVE adds up the busy cycles of the 8 XCDs: cycles per
+            # XCD over the dispatch's duration is the average shader clock, and
+            # the dense bf16 peak scales with it (2.5 PFLOP/s at 2.4 GHz).  Only
+            # for dispatches long enough (> 100 us) for the ratio to mean it.
+            ghz = cs["GRBM_GUI_ACTIVE"] / 8.0 / cs["duration_ns"]
+            print("    %-28s %.4g" % ("avg_clock_ghz", ghz))
+            print("    %-28s %.4g" % ("bf16_peak_at_clock_tflops", BF16_PEAK_TFLOPS * ghz / 2.4))
     for r in _read_kernel_stats(args.summarize_profile):
         print("%-80s calls %6s  avg %10.3f us  total %12.3f us  %6.2f%%" % (
             r["Name"][:80], r["Calls"], float(r["AverageNs"]) / 1e3,

@@ -99,14 +99,14 @@ enum Activation {
     ACT_SIGMOID = 2, // sigmoid(g)                 the GLU Gated MLP
 };
 
-// act(g) for a block-uniform activation.
+// act(g) for a block-uniform activation, without branches:
+// act(g) = a * sigmoid(beta * g) with a = g for silu and swish_beta and a = 1
+// for sigmoid.  The caller passes beta = 1 for silu and sigmoid, where the
+// product beta * g is then exactly g, so this is silu(g) bit for bit.
 __device__ __forceinline__ float gate_act(float g, int act, float beta)
 {
-    if (act == ACT_SILU)
-        return silu(g);
-    if (act == ACT_SWISH)
-        return g * __builtin_amdgcn_rcpf(1.0f + __expf(-(beta * g)));
-    return __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+    const float s = __builtin_amdgcn_rcpf(1.0f + __expf(-(beta * g)));
+    return (act == ACT_SIGMOID ? 1.0f : g) * s;
 }
 
 // Hardware places consecutive workgroups round-robin on the 8 XCDs (each with

@@ -489,37 +489,53 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         ds[ni] = EPI == EPI_STORE && p.rowdiv && t < N ? p.rowdiv[t] : 1.0f;
     }
     const bool divided = EPI == EPI_STORE && p.rowdiv;
+    // All of the wave's packed results first, each group of 4 columns into
+    // registers of its own, then the stores back to back: a store's data
+    // registers are not overwritten while it is in flight, so no store waits
+    // for an earlier one to complete.
+    u32x2 packed[TM][TN][4];
 #pragma unroll
     for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int f = m0 + wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-                if (t < N && f < M) {
-                    float v[4];
+                float v[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        if constexpr (EPI == EPI_GATE_MUL) {
-                            float g = acc[0][mi][ni][4 * j + e], u = acc[NW - 1][mi][ni][4 * j + e];
-                            if (scaled) {
-                                g *= rs[ni];
-                                u *= rs[ni];
-                            }
-                            v[e] = gate_act(g, p.activation, p.beta) * u;
-                        } else {
-                            v[e] = acc[0][mi][ni][4 * j + e];
-                            if (divided)
-                                v[e] = v[e] / ds[ni];
+                for (int e = 0; e < 4; ++e) {
+                    if constexpr (EPI == EPI_GATE_MUL) {
+                        float g = acc[0][mi][ni][4 * j + e], u = acc[NW - 1][mi][ni][4 * j + e];
+                        if (scaled) {
+                            g *= rs[ni];
+                            u *= rs[ni];
                         }
+                        v[e] = gate_act(g, p.activation, p.beta) * u;
+                    } else {
+                        v[e] = acc[0][mi][ni][4 * j + e];
+                        if (divided)
+                            v[e] = v[e] / ds[ni];
                     }
-                    u32x2 packed = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                    *(u32x2 *)(p.out + (size_t)t * M + f) = packed;
                 }
+                packed[mi][ni][j] = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
                 // Keep the scheduler from pulling every accumulator out of
                 // the AGPRs at once.
                 __builtin_amdgcn_sched_barrier(0);
+            }
+    // Unconditional buffer stores relative to the tile's corner: a lane
+    // whose element lies outside [N, M] stores at an offset past the buffer
+    // range, which the hardware drops.  The largest in-range offset,
+    // ((BN - 1) M + M - 4) * 2 bytes, stays below 2^31 for M <= 2^22.
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.out + (size_t)n0 * M + m0);
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
+                const uint32_t off = n0 + tl < N && m0 + fl < M ? (uint32_t)(tl * M + fl) * 2u : kOutOfRange;
+                __builtin_amdgcn_raw_buffer_store_b64(packed[mi][ni][j], ro, off, 0, 0);
             }
 }
 
