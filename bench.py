@@ -103,6 +103,8 @@ def parse_args(argv=None):
                         "softmax_matmul | softmax_matmul_tiny | all")
     p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
+    p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused"],
+                   help="kernel path of the Gated MLP step (fused: one cooperative kernel, T <= 8)")
     p.add_argument("--copies", type=int, default=0,
                    help="weight copies to rotate through (0: enough to exceed 1.1 GB "
                         "for memory-bound shapes, 1 otherwise)")
@@ -207,6 +209,7 @@ def run_workload(name, args):
     xp, yp, hp, wsp = P(x.data_ptr()), P(y.data_ptr()), P(h.data_ptr()), P(ws.buffer.data_ptr())
     wp = [tuple(P(t.data_ptr()) for t in s) for s in wsets]
     auto = gmlp.PATH_AUTO
+    path_id = gmlp._PATHS[args.path]
     variant = VARIANTS[args.variant]
     vargs = gmlp._variant(variant.get("activation", "silu"), variant.get("beta", 1.0),
                           variant.get("rmsnorm", False), variant.get("eps", 0.0))
@@ -214,8 +217,8 @@ def run_workload(name, args):
     def step(i):
         g, u, d = wp[i % copies]
         if not variant:
-            return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, auto, wsp, ws.nbytes, st)
-        return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, auto, wsp, ws.nbytes, st)
+            return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, path_id, wsp, ws.nbytes, st)
+        return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, path_id, wsp, ws.nbytes, st)
 
     def gate_up_only(i):
         g, u, _ = wp[i % copies]
@@ -254,7 +257,7 @@ def run_workload(name, args):
     k_kernel = max(args.steps, 20)
     gate_up_ms = timed(gate_up_only, k_kernel)
     down_ms = timed(down_only, k_kernel)
-    plan = gmlp.describe(T, D, F)
+    plan = gmlp.describe(T, D, F, args.path)
     stats = per_step_stats(step, k_kernel, stream)
     # Context only: every step on the same weight copy, which the 256 MB
     # Infinity Cache may then serve in part.
@@ -276,7 +279,7 @@ def run_workload(name, args):
         achieved, peak, r_unit = dom_bytes / (dom_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
     else:
         achieved, peak, r_unit = dom_flops / (dom_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
-    path = "gemv" if T <= 8 else "mfma"
+    path = args.path if args.path != "auto" else ("gemv" if T <= 8 else "mfma")
     props = torch.cuda.get_device_properties(dev)
     result = {
         "metric": METRIC,

@@ -59,9 +59,13 @@ enum gmlp_status {
 
 /* Which kernels compute the call (gmlp_forward_ex). */
 enum gmlp_path {
-    GMLP_PATH_AUTO = 0, /* GEMV for T <= 8, MFMA GEMMs otherwise */
-    GMLP_PATH_GEMV = 1, /* split-K streaming GEMV kernels; needs T <= 8 */
-    GMLP_PATH_MFMA = 2, /* MFMA GEMM kernels (any T) */
+    GMLP_PATH_AUTO = 0,  /* GEMV for T <= 8, MFMA GEMMs otherwise */
+    GMLP_PATH_GEMV = 1,  /* split-K streaming GEMV kernels; needs T <= 8 */
+    GMLP_PATH_MFMA = 2,  /* MFMA GEMM kernels (any T) */
+    GMLP_PATH_FUSED = 3, /* the whole MLP in one GEMV kernel: the first blocks run the gate/up
+                            items, the rest the down items, each waiting only for the strips
+                            of H its rows read; needs T <= 8; same Y as GMLP_PATH_GEMV bit for
+                            bit.  Only for gmlp_forward_ex / gmlp_forward_variant. */
 };
 
 /*
@@ -110,7 +114,8 @@ int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t b
 /*
  * Bytes of workspace gmlp_forward_ws / gmlp_forward_ex need for this shape
  * (for any path).  The workspace holds H [T, F] bf16, fp32 split-K partial
- * sums and a block of arrival counters.  0 if the shape is invalid.
+ * sums and a block of arrival counters and barrier flags.  0 if the shape is
+ * invalid.
  */
 size_t gmlp_workspace_size(int64_t T, int64_t D, int64_t F);
 

@@ -80,8 +80,20 @@ struct GemvShared {
 // streams the raw rows, adds up the squares of the activations it loads
 // anyway, and the last block of the strip scales G and U by
 // r = 1 / sqrt(sum(x^2) / K + eps) before the activation.
-template <int NT, int NW, int EPI, bool RMS>
-__device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh)
+struct NoWait {
+    __device__ void operator()() const {}
+};
+
+// One work item (a strip of columns times one split of rows).  Returns
+// whether this block wrote the strip's results (the only, or the last, split
+// of the strip).  CO writes the results with device-coherent stores and CX
+// reads the activations with device-coherent loads (the fused kernel hands H
+// from its gate/up blocks to its down blocks through them); with CX the
+// weights of the first batches are issued before wait() and the activations
+// only after it.
+template <int NT, int NW, int EPI, bool RMS, bool CO = false, bool CX = false, class Wait = NoWait>
+__device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh,
+                                          const Wait &wait = Wait{})
 {
     static_assert(!RMS || EPI == EPI_GATE_MUL, "RMSNorm belongs to the gate/up step");
     constexpr int RG = 8; // row groups per block
@@ -113,12 +125,13 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
     if constexpr (NW == 2)
         wp[1] = p.w1 + (size_t)kb * M + lcol;
     const uint16_t *xp = p.act + kb;
+    const __amdgpu_buffer_rsrc_t rxp = make_rsrc(xp); // CX: byte offsets stay below 2^27
     constexpr int XW = U / 2; // activation words (2 bf16 each) per token per batch
     struct Batch {
         uint32_t x[NT][XW];
         u32x4 w[U][NW];
     };
-    auto load_batch = [&](Batch &v, int b) __attribute__((always_inline)) {
+    auto load_x = [&](Batch &v, int b) __attribute__((always_inline)) {
         const int r0 = (8 * b + rg) * U;
         // Activation pieces of min(U, 8) rows lie wholly in or out of the
         // split (nrows is a multiple of 8, r0 of U).
@@ -128,24 +141,35 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
                 for (int q = 0; q < U / 8; ++q) {
                     const int r = r0 + 8 * q < nrows ? r0 + 8 * q : 0;
-                    const u32x4 x4 = *(const u32x4 *)(xp + (size_t)t * K + r);
+                    u32x4 x4;
+                    if constexpr (CX)
+                        x4 = __builtin_amdgcn_raw_buffer_load_b128(rxp, (uint32_t)(t * K + r) * 2u, 0, kCoherent);
+                    else
+                        x4 = *(const u32x4 *)(xp + (size_t)t * K + r);
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         v.x[t][4 * q + e] = x4[e];
                 }
             } else if constexpr (U == 4) {
                 const int r = r0 < nrows ? r0 : 0;
-                const u32x2 x2 = *(const u32x2 *)(xp + (size_t)t * K + r);
+                u32x2 x2;
+                if constexpr (CX)
+                    x2 = __builtin_amdgcn_raw_buffer_load_b64(rxp, (uint32_t)(t * K + r) * 2u, 0, kCoherent);
+                else
+                    x2 = *(const u32x2 *)(xp + (size_t)t * K + r);
                 v.x[t][0] = x2[0];
                 v.x[t][1] = x2[1];
             } else {
                 const int r = r0 < nrows ? r0 : 0;
-                v.x[t][0] = *(const uint32_t *)(xp + (size_t)t * K + r);
+                if constexpr (CX)
+                    v.x[t][0] = __builtin_amdgcn_raw_buffer_load_b32(rxp, (uint32_t)(t * K + r) * 2u, 0, kCoherent);
+                else
+                    v.x[t][0] = *(const uint32_t *)(xp + (size_t)t * K + r);
             }
         }
-        // The activations must be issued before the weights: loads complete
-        // in order, so waiting for a batch's weights then covers them too.
-        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto load_w = [&](Batch &v, int b) __attribute__((always_inline)) {
+        const int r0 = (8 * b + rg) * U;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int r = min(r0 + u, nrows - 1);
@@ -154,12 +178,30 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                 v.w[u][w] = __builtin_nontemporal_load((const u32x4 *)(wp[w] + (size_t)r * M));
         }
     };
+    auto load_batch = [&](Batch &v, int b) __attribute__((always_inline)) {
+        load_x(v, b);
+        // The activations must be issued before the weights: loads complete
+        // in order, so waiting for a batch's weights then covers them too.
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(v, b);
+    };
     constexpr int DEPTH = gemv_depth<NT>();
     const int nb = (nrows + RG * U - 1) / (RG * U);
     Batch ring[DEPTH];
+    // Prologue: DEPTH batches (past the split if i >= nb: never accumulated).
+    if constexpr (CX) {
 #pragma unroll
-    for (int i = 0; i < DEPTH; ++i)
-        load_batch(ring[i], i); // past the split if i >= nb (never accumulated)
+        for (int i = 0; i < DEPTH; ++i)
+            load_w(ring[i], i);
+        wait();
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i)
+            load_x(ring[i], i);
+    } else {
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i)
+            load_batch(ring[i], i);
+    }
 
     float acc[NW][NT][8];
     float ssq[NT]; // RMS: this row group's sum of x^2 per token
@@ -292,7 +334,7 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
         }
         __syncthreads();
         if (!sh.last)
-            return;
+            return false;
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if constexpr (RMS) {
@@ -381,9 +423,15 @@ __device__ __forceinline__ void gemv_item(const GemvParams &p, int item, GemvSha
                 if (p.rowdiv)
                     y = y / p.rowdiv[t];
             }
-            p.out[(size_t)t * M + m] = __builtin_bit_cast(uint16_t, (__bf16)y);
+            const uint16_t bits = __builtin_bit_cast(uint16_t, (__bf16)y);
+            if constexpr (CO)
+                __builtin_amdgcn_raw_buffer_store_b16(bits, make_rsrc(p.out), (uint32_t)(t * M + m) * 2u, 0,
+                                                      kCoherent);
+            else
+                p.out[(size_t)t * M + m] = bits;
         }
     }
+    return true;
 }
 
 // At most 256 VGPRs per lane: two blocks per CU stay resident.
@@ -393,6 +441,95 @@ void gemv_splitk_kernel(GemvParams p)
 {
     __shared__ GemvShared<NT, NW> sh;
     gemv_item<NT, NW, EPI, RMS>(p, blockIdx.x, sh);
+}
+
+// ---- one kernel for both steps (decode, T <= 8) -------------------------------
+
+struct GemvFusedParams {
+    GemvParams gate_up, down;    // down.counters must not overlap gate_up.counters
+    uint32_t *ready;             // per down split s: [kFlagStride*s] gate/up strips done that
+                                 // it needs, [kFlagStride*s + 1] down blocks past the wait
+                                 // (both zero on entry and exit)
+    uint32_t spin_limit;         // polls before a waiting block gives up
+};
+
+constexpr int kFusedMaxSplits = 512;
+constexpr int kFlagStride = 32; // words between the ready words of two splits: one 128-byte line each
+
+// Gate/up strips (of 8 * strip_lanes columns of H) that overlap the rows
+// [s * k_split, (s + 1) * k_split) of down split s.
+__device__ __forceinline__ uint32_t fused_strips_of_split(const GemvParams &gu, const GemvParams &dn, int s)
+{
+    const int width = 8 * gu.strip_lanes;
+    const int r0 = s * dn.k_split, r1 = min(dn.K, r0 + dn.k_split);
+    return (uint32_t)((r1 - 1) / width - r0 / width + 1);
+}
+
+// What a down block waits for: every gate/up strip its split reads is
+// written (its count is complete).  Thread 0 polls the split's own line;
+// the last of the split's down blocks to get past resets the words.  Only
+// blocks of lower index (dispatched earlier) are waited for, so the wait
+// ends whatever number of blocks the device holds at once; a block that
+// polls spin_limit times goes on regardless (no wave waits for ever).
+struct FusedWait {
+    uint32_t *w;         // the split's ready words
+    uint32_t need;       // gate/up strips the split reads
+    uint32_t consumers;  // down blocks of the split (its strips of Y)
+    uint32_t spin_limit;
+    __device__ void operator()() const
+    {
+        if (threadIdx.x == 0) {
+            for (uint32_t polls = 0;
+                 __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need && polls < spin_limit;
+                 ++polls)
+                __builtin_amdgcn_s_sleep(2);
+            const uint32_t past = __hip_atomic_fetch_add(w + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (past == consumers - 1) {
+                __hip_atomic_store(w, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(w + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        barrier_only();
+    }
+};
+
+// The whole Gated MLP for T <= 8 in one launch of n_gu + n_dn blocks:
+// blocks below n_gu run the gate/up items (H written through to memory with
+// device-coherent stores); the block that completes a strip of H then
+// counts it in for every down split that reads it.  The other blocks run the
+// down items: they issue their first weight loads, wait for their split's
+// strips of H, and read H with device-coherent loads.  Items and reductions
+// are those of the two-kernel GEMV path, so Y is bit for bit that path's.
+template <int NT, bool RMS>
+__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void gemv_fused_kernel(GemvFusedParams p)
+{
+    __shared__ union {
+        GemvShared<NT, 2> gate_up;
+        GemvShared<NT, 1> down;
+    } sh;
+    const int n_gu = p.gate_up.strips * p.gate_up.splits;
+    const int b = blockIdx.x;
+    if (b < n_gu) {
+        if (gemv_item<NT, 2, EPI_GATE_MUL, RMS, true>(p.gate_up, b, sh.gate_up)) {
+            wait_vmcnt<0>(); // this wave's part of the strip is written through
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                const int width = 8 * p.gate_up.strip_lanes;
+                const int j = b % p.gate_up.strips;
+                const int f0 = j * width, f1 = min(p.gate_up.M, f0 + width);
+                for (int s = f0 / p.down.k_split; s <= (f1 - 1) / p.down.k_split; ++s)
+                    __hip_atomic_fetch_add(p.ready + kFlagStride * s, 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        return;
+    }
+    const int item = b - n_gu;
+    const int split = item / p.down.strips;
+    const FusedWait wait{p.ready + kFlagStride * split, fused_strips_of_split(p.gate_up, p.down, split),
+                         (uint32_t)p.down.strips, p.spin_limit};
+    gemv_item<NT, 1, EPI_STORE, false, false, true>(p.down, item, sh.down, wait);
 }
 
 } // namespace gmlp

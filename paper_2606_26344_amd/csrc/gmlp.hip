@@ -65,9 +65,15 @@ constexpr int64_t kMaxTokens = int64_t(1) << 30;
 constexpr size_t kAlign = 256;
 // Arrival counters sit at the start of every workspace in a block of fixed
 // size (enough for any shape: at most kMaxDim / 256 GEMV strips, fewer than
-// 256 split GEMM tiles), so a zeroed workspace stays valid when it is reused
-// for another shape.
-constexpr size_t kCounterBytes = 64 * 1024;
+// 256 split GEMM tiles), followed by the fused kernel's ready words (one
+// 128-byte line per down split), so a zeroed workspace stays valid when it
+// is reused for another shape.  Every kernel leaves them zero.
+constexpr size_t kStripCounterBytes = 64 * 1024;
+constexpr size_t kReadyBytes = (size_t)kFusedMaxSplits * kFlagStride * sizeof(uint32_t);
+constexpr size_t kCounterBytes = kStripCounterBytes + kReadyBytes;
+// Polls of a ready word (each with a short sleep) before a down block of the
+// fused kernel stops waiting: about a second, far beyond any real wait.
+constexpr uint32_t kSpinLimit = 1u << 20;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -203,7 +209,7 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     if (path == GMLP_PATH_AUTO)
         path = T <= kGemvMaxTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
     p.path = path;
-    if (path == GMLP_PATH_GEMV) {
+    if (path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) {
         gemv_step(p.gate_up, (int)F, (int)T, (int)D, 2);
         gemv_step(p.down, (int)D, (int)T, (int)F, 1);
         return p;
@@ -232,6 +238,8 @@ Layout make_layout(int64_t T, int64_t D, int64_t F)
         const Plan p = make_plan(T, D, F, path);
         counters = std::max({counters, p.gate_up.counters, p.down.counters});
         partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes});
+        if (path == GMLP_PATH_GEMV) // the fused kernel runs both steps at once: separate partial sums
+            partial = std::max(partial, align_up(p.gate_up.partial_bytes) + p.down.partial_bytes);
     }
     Layout l;
     l.counters_off = 0;
@@ -434,6 +442,48 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
     }
 }
 
+// The fused kernel: the gate/up items on the first blocks, the down items on
+// the rest, all in one launch.
+int fused_grid(const Plan &plan) { return plan.gate_up.blocks + plan.down.blocks; }
+
+template <int NT, bool RMS>
+int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                    uint8_t *ws, const Layout &l, const Variant &v, hipStream_t st)
+{
+    if (plan.down.splits > kFusedMaxSplits)
+        return fail(GMLP_ERR_UNSUPPORTED, "fused path: %d down splits, at most %d", plan.down.splits,
+                    kFusedMaxSplits);
+    if ((size_t)(plan.gate_up.strips + plan.down.strips) * sizeof(uint32_t) > kStripCounterBytes)
+        return fail(GMLP_ERR_UNSUPPORTED, "fused path: too many strips for the counter block");
+    void *H = ws + l.h_off;
+    GemvFusedParams fp;
+    fp.gate_up = gemv_params(plan.gate_up, Wg, Wu, X, H, ws, l, v, nullptr);
+    fp.down = gemv_params(plan.down, Wd, nullptr, H, Y, ws, l, Variant{}, nullptr);
+    fp.down.counters = fp.gate_up.counters + plan.gate_up.strips;
+    fp.down.partial = reinterpret_cast<float *>(ws + l.partial_off + align_up(plan.gate_up.partial_bytes));
+    fp.ready = reinterpret_cast<uint32_t *>(ws + l.counters_off + kStripCounterBytes);
+    fp.spin_limit = kSpinLimit;
+    hipLaunchKernelGGL((gemv_fused_kernel<NT, RMS>), dim3(fused_grid(plan)), dim3(kGemvThreads), 0, st, fp);
+    return hip_check(hipGetLastError(), "fused kernel launch");
+}
+
+template <bool RMS>
+int launch_fused(const Plan &plan, const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                 uint8_t *ws, const Layout &l, const Variant &v, hipStream_t st)
+{
+    switch (plan.gate_up.N) {
+    case 1: return launch_fused_nt<1, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 2: return launch_fused_nt<2, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 3: return launch_fused_nt<3, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 4: return launch_fused_nt<4, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 5: return launch_fused_nt<5, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 6: return launch_fused_nt<6, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 7: return launch_fused_nt<7, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    case 8: return launch_fused_nt<8, RMS>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+    default: return fail(GMLP_ERR_INVALID_ARG, "fused path needs 1 <= T <= 8 (T=%d)", plan.gate_up.N);
+    }
+}
+
 int check_variant(int activation, float beta, int rmsnorm, float eps, Variant *v)
 {
     if (activation != GMLP_ACT_SILU && activation != GMLP_ACT_SWISH && activation != GMLP_ACT_SIGMOID)
@@ -453,12 +503,21 @@ int check_variant(int activation, float beta, int rmsnorm, float eps, Variant *v
 
 int check_path(int path, int64_t T)
 {
-    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA)
+    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA && path != GMLP_PATH_FUSED)
         return fail(GMLP_ERR_INVALID_ARG, "unknown path %d", path);
-    if (path == GMLP_PATH_GEMV && T > kGemvMaxTokens)
-        return fail(GMLP_ERR_UNSUPPORTED, "GEMV path needs T <= %d (T=%lld)", kGemvMaxTokens,
-                    (long long)T);
+    if ((path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) && T > kGemvMaxTokens)
+        return fail(GMLP_ERR_UNSUPPORTED, "%s path needs T <= %d (T=%lld)",
+                    path == GMLP_PATH_GEMV ? "GEMV" : "fused", kGemvMaxTokens, (long long)T);
     return GMLP_OK;
+}
+
+// The entry points that run one step alone (and Softmax+MatMul) have no
+// fused form.
+int check_single_step_path(int path, int64_t T)
+{
+    if (path == GMLP_PATH_FUSED)
+        return fail(GMLP_ERR_UNSUPPORTED, "the fused path runs the whole Gated MLP only");
+    return check_path(path, T);
 }
 
 int check_workspace(void *ws, size_t ws_bytes, const Layout &l)
@@ -469,7 +528,7 @@ int check_workspace(void *ws, size_t ws_bytes, const Layout &l)
         return fail(GMLP_ERR_UNSUPPORTED, "workspace %p is not %zu-byte aligned", ws, kAlign);
     if (ws_bytes < l.total)
         return fail(GMLP_ERR_NO_MEMORY, "workspace of %zu bytes, %zu needed", ws_bytes, l.total);
-    if ((size_t)l.counters * sizeof(uint32_t) > kCounterBytes)
+    if ((size_t)l.counters * sizeof(uint32_t) > kStripCounterBytes)
         return fail(GMLP_ERR_UNSUPPORTED, "shape needs %d arrival counters, more than the %zu reserved",
                     l.counters, kCounterBytes / sizeof(uint32_t));
     return GMLP_OK;
@@ -562,6 +621,12 @@ int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t b
         snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", name, blocks, threads, splits);
         text += tmp;
     };
+    if (plan.path == GMLP_PATH_FUSED) {
+        const std::string name = "gemv_fused_kernel<" + std::to_string(T) + ", false>";
+        line(name.c_str(), fused_grid(plan), kGemvThreads, plan.gate_up.splits);
+        snprintf(buf, bytes, "%s", text.c_str());
+        return ok();
+    }
     for (const Step *s : {&plan.gate_up, &plan.down}) {
         const std::string name = kernel_name(*s, s == &plan.gate_up);
         line(name.c_str(), s->blocks, s->threads, s->splits);
@@ -605,6 +670,11 @@ int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const vo
     const Plan plan = make_plan(T, D, F, path);
     uint8_t *ws = static_cast<uint8_t *>(workspace);
     hipStream_t st = static_cast<hipStream_t>(stream);
+    if (plan.path == GMLP_PATH_FUSED) {
+        rc = v.rms ? launch_fused<true>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st)
+                   : launch_fused<false>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+        return rc ? rc : ok();
+    }
     void *H = ws + l.h_off;
     if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, ws, l, v, st)) ||
         (rc = run_down(plan.down, H, Wd, Y, ws, l, st)))
@@ -680,7 +750,7 @@ int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H,
 {
     int rc;
     Variant v;
-    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)) || (rc = check_path(path, T)) ||
+    if ((rc = check_gate_up_args(X, Wg, Wu, H, T, D, F)) || (rc = check_single_step_path(path, T)) ||
         (rc = check_variant(activation, beta, rmsnorm, eps, &v)))
         return rc;
     if (T == 0)
@@ -706,7 +776,7 @@ int gmlp_down_ws(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, i
                  void *workspace, size_t ws_bytes, void *stream)
 {
     int rc;
-    if ((rc = check_down_args(H, Wd, Y, T, F, D)) || (rc = check_path(path, T)))
+    if ((rc = check_down_args(H, Wd, Y, T, F, D)) || (rc = check_single_step_path(path, T)))
         return rc;
     if (T == 0)
         return ok();
@@ -849,7 +919,7 @@ int softmax_matmul_describe(int64_t M, int64_t K, int64_t N, int path, char *buf
     buf[0] = '\0';
     if ((rc = check_smm_shape(M, K, N)))
         return rc;
-    if ((rc = check_path(path, M)))
+    if ((rc = check_single_step_path(path, M)))
         return rc;
     if (M == 0)
         return ok();
@@ -865,7 +935,7 @@ int softmax_matmul_ws(const void *X, const void *Y, void *Z, int64_t M, int64_t 
                       void *workspace, size_t ws_bytes, void *stream)
 {
     int rc;
-    if ((rc = check_smm_args(X, Y, Z, M, K, N)) || (rc = check_path(path, M)))
+    if ((rc = check_smm_args(X, Y, Z, M, K, N)) || (rc = check_single_step_path(path, M)))
         return rc;
     if (M == 0)
         return ok();
@@ -907,7 +977,7 @@ int softmax_matmul_divide_ws(const void *P, const float *s, const void *Y, void 
                              int64_t N, int path, void *workspace, size_t ws_bytes, void *stream)
 {
     int rc;
-    if ((rc = check_smm_args(P, Y, Z, M, K, N)) || (rc = check_path(path, M)))
+    if ((rc = check_smm_args(P, Y, Z, M, K, N)) || (rc = check_single_step_path(path, M)))
         return rc;
     if (M > 0 && !s)
         return fail(GMLP_ERR_INVALID_ARG, "s is NULL");

@@ -114,7 +114,7 @@ def test_describe_rejects_bad_arguments(lib):
     buf = ctypes.create_string_buffer(64)
     assert lib.gmlp_describe(4, 260, 512, 0, buf, 64) == 2
     assert lib.gmlp_describe(9, 256, 512, 1, buf, 64) == 2  # GEMV needs T <= 8
-    assert lib.gmlp_describe(4, 256, 512, 3, buf, 64) == 1  # unknown path
+    assert lib.gmlp_describe(4, 256, 512, 4, buf, 64) == 1  # unknown path
     assert lib.gmlp_describe(4, 256, 512, 0, None, 64) == 1
     assert lib.gmlp_describe(4, 256, 512, 0, buf, 8) == 0 and len(buf.value) == 7  # truncated
 
@@ -212,3 +212,30 @@ def test_softmax_matmul_halves_validate_before_launching(lib):
     assert div(P, S, Y, S, 4, 256, 512, 0, W, n, None) == 1   # Z on s
     assert div(P, S, Y, Z, 4, 256, 512, 0, W, n - 256, None) == 4
     assert div(P, S, Y, Z, 9, 256, 512, 1, W, n, None) == 2   # GEMV needs M <= 8
+
+
+def test_fused_path_plan_and_validation(lib):
+    fused = gmlp.describe(1, 4096, 14336, "fused")
+    gemv = gmlp.describe(1, 4096, 14336, "gemv")
+    assert len(fused) == 1 and fused[0][0] == "gemv_fused_kernel<1, false>"
+    # One block per item of either step: the gate/up items first.
+    assert fused[0][1] == sum(g[1] for g in gemv) and fused[0][2] == 256
+    assert fused[0][3] == gemv[0][3]
+    for T in range(1, 9):
+        (name, grid, block, splits), = gmlp.describe(T, 264, 520, "fused")
+        assert name == "gemv_fused_kernel<%d, false>" % T
+        assert grid == sum(g[1] for g in gmlp.describe(T, 264, 520, "gemv"))
+    buf = ctypes.create_string_buffer(64)
+    assert lib.gmlp_describe(9, 256, 512, 3, buf, 64) == 2  # fused needs T <= 8
+    n = gmlp.workspace_size(4, 256, 512)
+    args = (A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, 9, 256, 512)
+    assert lib.gmlp_forward_ex(*args, 3, A + 300 * MB, n, None) == 2
+    # The single-step entry points and Softmax+MatMul have no fused form.
+    assert lib.gmlp_gate_up_ws(A, A + 64 * MB, A + 128 * MB, A + 192 * MB, 4, 256, 512, 3,
+                               A + 300 * MB, n, None) == 2
+    assert lib.gmlp_down_ws(A, A + 64 * MB, A + 128 * MB, 4, 512, 256, 3, A + 300 * MB, n,
+                            None) == 2
+    m = smm.workspace_size(4, 256, 512)
+    assert lib.softmax_matmul_ws(A, A + 64 * MB, A + 128 * MB, 4, 256, 512, 3, A + 192 * MB, m,
+                                 None) == 2
+    assert "fused" in gmlp.last_error()

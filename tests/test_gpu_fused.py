@@ -1,0 +1,85 @@
+"""GPU checks of the fused decode kernel (GMLP_PATH_FUSED): the whole Gated
+MLP for T <= 8 in one cooperative launch with a grid-wide barrier between
+the gate/up and the down items.
+
+It runs the same items and reductions as the two-kernel GEMV path, so its Y
+must equal that path's bit for bit; it is also held to the oracle's
+tolerance |Y - Y_ref| <= 1e-2 (|Y_ref| + rms(Y_ref)).
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_26344_amd import gmlp
+from paper_2606_26344_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    gmlp.library()
+
+
+def _run(X, Wg, Wu, Wd, path, ws=None, **variant):
+    y = gmlp.forward(*(gmlp.from_bf16_bits(a) for a in (X, Wg, Wu, Wd)), path=path, workspace=ws,
+                     **variant)
+    torch.cuda.synchronize()
+    return gmlp.to_bf16_bits(y)
+
+
+def _check(got_bits, ref, what):
+    got = I.bf16_bits_to_f32(got_bits).astype(np.float64)
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    err = np.abs(got - ref)
+    bound = TOL * (np.abs(ref) + rms)
+    ratio = float(np.max(err / bound))
+    print("%s max err/bound = %.3f" % (what, ratio), flush=True)
+    assert np.all(err <= bound), what
+
+
+SHAPES = [(T, 264, 520) for T in range(1, 9)] + [(1, 72, 136), (5, 1032, 72), (8, 2056, 1032)]
+
+
+@pytest.mark.parametrize("T,D,F", SHAPES, ids=["T%dD%dF%d" % s for s in SHAPES])
+def test_fused_equals_two_kernels_and_oracle(orc, T, D, F):
+    print("fused T=%d D=%d F=%d" % (T, D, F), flush=True)
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=100 + T + D)
+    fused = _run(X, Wg, Wu, Wd, "fused")
+    assert np.array_equal(fused, _run(X, Wg, Wu, Wd, "gemv"))
+    _check(fused, orc.gated_mlp_rows(X, Wg, Wu, Wd), "fused T=%d D=%d F=%d" % (T, D, F))
+
+
+@pytest.mark.parametrize("T", [1, 2, 8])
+def test_fused_decode_shape(orc, T):
+    print("fused decode T=%d" % T, flush=True)
+    X, Wg, Wu, Wd = I.generate(T, 4096, 14336, seed=T)
+    fused = _run(X, Wg, Wu, Wd, "fused")
+    assert np.array_equal(fused, _run(X, Wg, Wu, Wd, "gemv"))
+    _check(fused, orc.gated_mlp_rows(X, Wg, Wu, Wd), "fused decode T=%d" % T)
+
+
+@pytest.mark.parametrize("variant", [dict(rmsnorm=True, eps=1e-5),
+                                     dict(activation="swish", beta=1.702, rmsnorm=True, eps=1e-6),
+                                     dict(activation="sigmoid")],
+                         ids=["rmsnorm", "rmsnorm_swiglu", "glu"])
+def test_fused_variants(orc, variant):
+    X, Wg, Wu, Wd = I.generate(3, 1032, 2056, seed=7)
+    fused = _run(X, Wg, Wu, Wd, "fused", **variant)
+    assert np.array_equal(fused, _run(X, Wg, Wu, Wd, "gemv", **variant))
+    _check(fused, orc.gated_mlp_rows(X, Wg, Wu, Wd, **variant), "fused %s" % variant)
+
+
+def test_fused_repeated_calls_on_one_workspace():
+    # The barrier's count and flags return to zero: back-to-back calls, and a
+    # call of another shape in between, give the same bits.
+    X, Wg, Wu, Wd = I.generate(4, 1032, 2056, seed=9)
+    X2, Wg2, Wu2, Wd2 = I.generate(2, 264, 520, seed=10)
+    ws = gmlp.Workspace(4, 1032, 2056)
+    first = _run(X, Wg, Wu, Wd, "fused", ws)
+    for _ in range(3):
+        _run(X2, Wg2, Wu2, Wd2, "fused", ws)
+        assert np.array_equal(_run(X, Wg, Wu, Wd, "fused", ws), first)
