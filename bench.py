@@ -105,6 +105,9 @@ def parse_args(argv=None):
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
     p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused"],
                    help="kernel path of the Gated MLP step (fused: one cooperative kernel, T <= 8)")
+    p.add_argument("--graph", action="store_true",
+                   help="also time the step captured in a HIP graph (one step per weight copy, "
+                        "replayed; context for launch overhead)")
     p.add_argument("--copies", type=int, default=0,
                    help="weight copies to rotate through (0: enough to exceed 1.1 GB "
                         "for memory-bound shapes, 1 otherwise)")
@@ -214,11 +217,12 @@ def run_workload(name, args):
     vargs = gmlp._variant(variant.get("activation", "silu"), variant.get("beta", 1.0),
                           variant.get("rmsnorm", False), variant.get("eps", 0.0))
 
-    def step(i):
+    def step(i, stream_ptr=st):
         g, u, d = wp[i % copies]
         if not variant:
-            return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, path_id, wsp, ws.nbytes, st)
-        return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, path_id, wsp, ws.nbytes, st)
+            return lib.gmlp_forward_ex(xp, g, u, d, yp, T, D, F, path_id, wsp, ws.nbytes, stream_ptr)
+        return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, path_id, wsp, ws.nbytes,
+                                        stream_ptr)
 
     def gate_up_only(i):
         g, u, _ = wp[i % copies]
@@ -262,6 +266,7 @@ def run_workload(name, args):
     # Context only: every step on the same weight copy, which the 256 MB
     # Infinity Cache may then serve in part.
     unrotated_ms = timed(lambda i: step(0), k_kernel) if copies > 1 else None
+    graph_ms = graph_step_ms(step, copies, args.steps, dev) if args.graph else None
 
     sec = ms_per_step / 1e3
     if bound == "hbm":
@@ -326,6 +331,7 @@ def run_workload(name, args):
             "wall_s": round(wall, 4),
             "single_steps": stats,
             "unrotated_weights_us": None if unrotated_ms is None else round(unrotated_ms * 1e3, 3),
+            "graph_replay_us": None if graph_ms is None else round(graph_ms * 1e3, 3),
         },
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "arch": getattr(props, "gcnArchName", "")},
@@ -371,6 +377,40 @@ def per_step_stats(fn, k, stream):
     us = [a.elapsed_time(b) * 1e3 for a, b in evs]
     return {"median_us": round(statistics.median(us), 3), "mean_us": round(statistics.fmean(us), 3),
             "min_us": round(min(us), 3), "steps": k}
+
+
+def graph_step_ms(step, copies, k, dev):
+    """ms per step of `copies` steps (one per weight copy) captured in one HIP
+    graph on a side stream and replayed until about k steps have run."""
+    import ctypes
+
+    import torch
+
+    side = torch.cuda.Stream(device=dev)
+    sp = ctypes.c_void_p(side.cuda_stream)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        for i in range(copies):
+            if step(i, sp):
+                raise RuntimeError("step failed before capture")
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        for i in range(copies):
+            step(i, sp)
+    reps = max(1, k // copies)
+    with torch.cuda.stream(side):
+        graph.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(side):
+        start.record(side)
+        for _ in range(reps):
+            graph.replay()
+        end.record(side)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / (reps * copies)
 
 
 def smm_algorithmic(M, K, N):
