@@ -19,11 +19,11 @@ Prints one JSON line per workload (the default workload is the T=1 decode
 shape) with:
   value      whole-job throughput: GB/s of algorithmic bytes 2(3DF + 2TD)
              for memory-bound shapes, TFLOP/s of 6TDF for compute-bound ones;
-  roofline   the dominant kernel (the gate/up kernel) launched on its own
-             and timed with HIP events on the library's stream: its
-             algorithmic bytes or flops per launch over its average
-             duration, against the MI355X peak (8 TB/s HBM, 2.5 PFLOP/s
-             dense bf16);
+  roofline   the dominant kernel (the gate/up kernel; with --path fused
+             the one kernel, i.e. the step) launched on its own and timed
+             with HIP events on the library's stream: its algorithmic bytes
+             or flops per launch over its average duration, against the
+             MI355X peak (8 TB/s HBM, 2.5 PFLOP/s dense bf16);
   cpu_baseline  the CPU fp64 oracle on this host's cores, on a bounded
              sample of the same workload, scaled to the same unit.
 --variant selects a member of the Gated MLP family (default: the SiLU Gated
@@ -33,7 +33,10 @@ RMSNorm of X in front (eps 1e-6), rmsnorm_swiglu = both.
 the second workload, Z = softmax(X) Y computed as (exp(X - rowmax) Y) / rowsum
 (one exp/row-sum kernel, then the matmul with the divide in its epilogue):
 value in TFLOP/s of 2MKN, the matmul kernel as the dominant one.
-Only one GPU is used: --gpus above 1 exits with a message.
+--path picks the kernel path (auto, gemv, mfma, or fused: the one-kernel
+decode path); --graph adds the step's time when captured in a HIP graph and
+replayed; --vendor-gemm adds the vendor library's time for the same matmul
+shapes (context).  Only one GPU is used: --gpus above 1 exits with a message.
 """
 from __future__ import annotations
 
@@ -67,15 +70,20 @@ CSRC = os.path.join(HERE, "paper_2606_26344_amd", "csrc")
 
 
 def kernel_source_sha256():
-    """Hash of the HIP sources: a traffic record is only valid for the
-    kernels it was measured on."""
+    """Hash of the HIP sources without their comments and whitespace: a
+    traffic record is only valid for the kernels it was measured on."""
     import hashlib
+    import re
 
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
         if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(CSRC, name), "rb") as fh:
-                h.update(name.encode() + b"\0" + fh.read())
+            with open(os.path.join(CSRC, name)) as fh:
+                code = fh.read()
+            code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+            code = re.sub(r"//[^\n]*", " ", code)
+            code = " ".join(code.split())
+            h.update(name.encode() + b"\0" + code.encode())
     return h.hexdigest()
 
 

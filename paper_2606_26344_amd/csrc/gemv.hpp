@@ -15,14 +15,15 @@
 //     the wave by a lane shuffle, across the 4 waves through LDS, and across
 //     the split-K items of a strip by the last block to finish (arrival
 //     counter), which adds the per-item sums in split order;
-//   * each lane keeps two or three batches of 16-byte weight loads in
-//     flight (a batch is reissued as soon as it has been consumed).
+//   * each lane keeps two batches of 16-byte weight loads in flight (a
+//     batch is reissued as soon as it has been consumed).
 //   The result is therefore bitwise reproducible run to run.
 //
 // The gate/up kernel (NW = 2) streams Wg and Wu together and its last block
 // applies H = bf16(act(G) * U) (act = silu, swish_beta or sigmoid; with
 // RMSNorm, G and U are first scaled by the row's r); the down kernel (NW = 1)
-// streams Wd and writes Y = bf16(H Wd).
+// streams Wd and writes Y = bf16(H Wd).  gemv_fused_kernel (end of file)
+// runs the items of both in one launch.
 #pragma once
 
 #include "common.hpp"
