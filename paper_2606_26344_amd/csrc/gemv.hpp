@@ -54,6 +54,11 @@ struct GemvParams {
     const float *rowdiv;
 };
 
+// Splits whose partial sums the last block of a strip loads at once: about
+// 16 values per thread in flight (NT * NW per split), so few round trips.
+template <int NT, int NW>
+constexpr int gemv_reduce_batch() { return NT * NW <= 1 ? 16 : NT * NW <= 2 ? 8 : NT * NW <= 4 ? 4 : 2; }
+
 constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
 constexpr int kGemvThreads = 256;
 
@@ -341,7 +346,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
         if constexpr (RMS) {
             // The whole row's sum of squares, splits added in order, with
             // the same unconditional loads as the column sums.
-            constexpr int C = NT <= 2 ? 4 : 2;
+            constexpr int C = gemv_reduce_batch<NT, NW>();
             float tot[NT];
             for (int s0 = 0; s0 < p.splits; s0 += C) {
                 float x[C][NT];
@@ -371,7 +376,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
             // in flight at once.  They are unconditional (a slot past the
             // last split reloads this block's own), so there are no
             // branches; the values past the last split are not added.
-            constexpr int C = NT <= 2 ? 4 : 2;
+            constexpr int C = gemv_reduce_batch<NT, NW>();
             const size_t stride = (size_t)NW * NT * M;
             const float *src = &p.partial[m];
             float sum[NW][NT];
