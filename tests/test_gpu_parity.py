@@ -193,3 +193,11 @@ def test_full_size_workload(orc, name, nrows):
     w = I.WORKLOADS[name]
     rows = None if nrows is None else I.sample_rows(w.T, nrows)
     _run(w.T, w.D, w.F, seed=w.seed, rows=rows, unit_rms=w.unit_rms_rows, orc=orc)
+
+
+@pytest.mark.parametrize("T,D,F", [(257, 264, 12296), (300, 136, 24584), (513, 264, 12296)])
+def test_large_gate_up_tiles_above_256_tokens(orc, T, D, F):
+    # Above 256 tokens the 256-token gate/up tiles are used once they nearly
+    # fill the chip; ragged token tails and column tails on that path.
+    assert gmlp.describe(T, D, F)[0][0].startswith("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4,")
+    _run(T, D, F, seed=T + F, orc=orc)
