@@ -105,7 +105,7 @@ struct GemmShape {
                   "every thread issues whole 16-byte loads");
     static_assert(STAGES >= 2 && STAGES <= 8, "2..8 LDS stages");
     static_assert((STAGES - 2) * LOADS_PER_STAGE < 64, "vmcnt range");
-    static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS capacity of a CU");
+    static_assert(STAGES * STAGE_BYTES + 256 <= 160 * 1024, "LDS capacity of a CU (with the kernel's other shared words)");
 };
 
 // Physical 16-byte chunk of logical chunk c in row k of a weight tile.  The
