@@ -343,45 +343,18 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
             return false;
         if (tid == 0)
             __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if constexpr (RMS) {
-            // The whole row's sum of squares, splits added in order, with
-            // the same unconditional loads as the column sums.
-            constexpr int C = gemv_reduce_batch<NT, NW>();
-            float tot[NT];
-            for (int s0 = 0; s0 < p.splits; s0 += C) {
-                float x[C][NT];
-#pragma unroll
-                for (int u = 0; u < C; ++u) {
-                    const int sp = s0 + u < p.splits ? s0 + u : split;
-#pragma unroll
-                    for (int t = 0; t < NT; ++t)
-                        x[u][t] = __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-#pragma unroll
-                for (int u = 0; u < C; ++u) {
-                    const int sp = s0 + u;
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const float xv = sp == split ? ss[t] : x[u][t];
-                        tot[t] = sp == 0 ? xv : sp < p.splits ? tot[t] + xv : tot[t];
-                    }
-                }
-            }
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-                ss[t] = tot[t];
-        }
         if (mvalid) {
             // Sum the splits in order 0, 1, 2, ...; the loads of C splits are
-            // in flight at once.  They are unconditional (a slot past the
-            // last split reloads this block's own), so there are no
-            // branches; the values past the last split are not added.
+            // in flight at once (with RMSNorm, their sums of x^2 too, added
+            // the same way).  They are unconditional (a slot past the last
+            // split reloads this block's own), so there are no branches; the
+            // values past the last split are not added.
             constexpr int C = gemv_reduce_batch<NT, NW>();
             const size_t stride = (size_t)NW * NT * M;
             const float *src = &p.partial[m];
-            float sum[NW][NT];
+            float sum[NW][NT], tot[NT];
             for (int s0 = 0; s0 < p.splits; s0 += C) {
-                float x[C][NW][NT];
+                float x[C][NW][NT], q[C][NT];
 #pragma unroll
                 for (int u = 0; u < C; ++u) {
                     const int sp = s0 + u < p.splits ? s0 + u : split;
@@ -391,6 +364,11 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                         for (int t = 0; t < NT; ++t)
                             x[u][w][t] = __hip_atomic_load(src + sp * stride + ((size_t)w * NT + t) * M,
                                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if constexpr (RMS)
+#pragma unroll
+                        for (int t = 0; t < NT; ++t)
+                            q[u][t] = __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
                 }
 #pragma unroll
                 for (int u = 0; u < C; ++u) {
@@ -402,6 +380,12 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                             const float xv = sp == split ? v[w][t] : x[u][w][t];
                             sum[w][t] = sp == 0 ? xv : sp < p.splits ? sum[w][t] + xv : sum[w][t];
                         }
+                    if constexpr (RMS)
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+                            const float qv = sp == split ? ss[t] : q[u][t];
+                            tot[t] = sp == 0 ? qv : sp < p.splits ? tot[t] + qv : tot[t];
+                        }
                 }
             }
 #pragma unroll
@@ -409,6 +393,10 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
                     v[w][t] = sum[w][t];
+            if constexpr (RMS)
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    ss[t] = tot[t];
         }
     }
 
