@@ -46,7 +46,7 @@ struct GemvParams {
     int activation;
     float beta;
     // RMSNorm (gate/up kernel with RMS = true): eps, and per-split sums of
-    // squares of the activations [splits][NT] fp32 when splits > 1.
+    // squares of the activations [strips][splits][NT] fp32 when splits > 1.
     float eps;
     float *ssq;
     // Store kernel: per-token divisors [NT] (nullptr: none), the softmax sums
@@ -327,9 +327,11 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                     __hip_atomic_store(&p.partial[(((size_t)split * NW + w) * NT + t) * M + m], v[w][t],
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
+        // Every strip of a split sums the same rows' x^2: each strip keeps
+        // its own copy, so no two blocks store to the same word.
         if constexpr (RMS)
             if (tid < NT)
-                __hip_atomic_store(&p.ssq[split * NT + tid], ss[tid], __ATOMIC_RELAXED,
+                __hip_atomic_store(&p.ssq[(strip * p.splits + split) * NT + tid], ss[tid], __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
         wait_vmcnt<0>();
         __syncthreads();
@@ -367,8 +369,8 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                     if constexpr (RMS)
 #pragma unroll
                         for (int t = 0; t < NT; ++t)
-                            q[u][t] = __hip_atomic_load(&p.ssq[sp * NT + t], __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
+                            q[u][t] = __hip_atomic_load(&p.ssq[(strip * p.splits + sp) * NT + t],
+                                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
 #pragma unroll
                 for (int u = 0; u < C; ++u) {

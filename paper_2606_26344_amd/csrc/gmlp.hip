@@ -199,8 +199,9 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.splits = (int)cdiv(K, rows);
     s.blocks = s.strips * s.splits;
     s.counters = s.splits > 1 ? s.strips : 0;
-    // Per-split column sums, then (gate/up) per-split sums of squares of X.
-    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * (nw * N * M + N) * sizeof(float) : 0;
+    // Per-split column sums, then (gate/up with RMSNorm) per-strip, per-split
+    // sums of squares of X.
+    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * ((size_t)nw * N * M + (size_t)s.strips * N) * sizeof(float) : 0;
 }
 
 Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
