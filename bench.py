@@ -112,7 +112,7 @@ def parse_args(argv=None):
     p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
     p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused"],
-                   help="kernel path of the Gated MLP step (fused: one cooperative kernel, T <= 8)")
+                   help="kernel path of the Gated MLP step (fused: both steps in one kernel, T <= 8)")
     p.add_argument("--graph", action="store_true",
                    help="also time the step captured in a HIP graph (one step per weight copy, "
                         "replayed; context for launch overhead)")

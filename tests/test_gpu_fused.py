@@ -1,6 +1,7 @@
 """GPU checks of the fused decode kernel (GMLP_PATH_FUSED): the whole Gated
-MLP for T <= 8 in one cooperative launch with a grid-wide barrier between
-the gate/up and the down items.
+MLP for T <= 8 in one launch, the gate/up items on the first blocks and the
+down items on the rest, each down block waiting only for the strips of H
+its rows read.
 
 It runs the same items and reductions as the two-kernel GEMV path, so its Y
 must equal that path's bit for bit; it is also held to the oracle's
