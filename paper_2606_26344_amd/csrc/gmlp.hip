@@ -236,6 +236,9 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
 // fits whichever kernels run.
 Layout make_layout(int64_t T, int64_t D, int64_t F)
 {
+    // T = 0 launches nothing; its workspace is sized as for one token (the
+    // plans below need at least one token tile).
+    T = std::max<int64_t>(T, 1);
     int counters = 0;
     size_t partial = 0;
     for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {
@@ -870,6 +873,7 @@ Step smm_matmul_step(int64_t M, int64_t K, int64_t N, int path) { return make_pl
 // every path of the shape.
 Layout smm_layout(int64_t M, int64_t K, int64_t N)
 {
+    M = std::max<int64_t>(M, 1); // as for make_layout: M = 0 launches nothing
     int counters = 0;
     size_t partial = 0;
     for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {

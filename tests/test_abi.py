@@ -6,6 +6,7 @@ import ctypes
 import pytest
 
 from paper_2606_26344_amd import gmlp
+from paper_2606_26344_amd import softmax_matmul as smm
 
 A = 0x10000000  # fake, 256-byte aligned addresses: validation never dereferences
 MB = 1 << 20
@@ -67,6 +68,10 @@ def test_validate_rejects_aliasing_output(lib):
 
 
 def test_workspace_size(lib):
+    # T = 0 is a valid shape (a call launches nothing); sizing it must not
+    # divide by the empty token-tile count.
+    assert gmlp.workspace_size(0, 256, 512) > 0
+    assert smm.workspace_size(0, 256, 512) > 0
     assert gmlp.workspace_size(16, 256, 512) > 0
     assert gmlp.workspace_size(4096, 4096, 14336) >= 4096 * 14336 * 2  # holds H
     assert gmlp.workspace_size(1, 4096, 14336) > 0
@@ -153,7 +158,6 @@ def test_variant_entry_points_validate_before_launching(lib):
 
 
 # ---- Softmax+MatMul (include/softmax_matmul.h) --------------------------------
-from paper_2606_26344_amd import softmax_matmul as smm  # noqa: E402
 
 
 def test_softmax_matmul_describe_names_the_kernels(lib):

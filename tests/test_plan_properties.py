@@ -1,0 +1,92 @@
+"""Randomised host-side checks of the kernel plans (no GPU): for shapes drawn
+over the supported range, gmlp_describe and softmax_matmul_describe give
+plans whose grids cover the problem, whose split-K splits cover the
+contracted axis, and whose workspace fits, and every entry point rejects
+what it must before touching a device."""
+import ctypes
+
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from paper_2606_26344_amd import gmlp
+from paper_2606_26344_amd import softmax_matmul as smm
+
+dims = st.integers(min_value=1, max_value=4096).map(lambda v: 8 * v)  # multiples of 8, up to 32768
+tokens = st.one_of(st.integers(min_value=1, max_value=8), st.integers(min_value=9, max_value=20000))
+
+
+def _cdiv(a, b):
+    return -(-a // b)
+
+
+def _tile(name):
+    # GemmShape<NW, WM, WN, TM, TN, STAGES, BK> -> (columns per weight, tokens per tile)
+    args = [int(v) for v in name.split("GemmShape<")[1].split(">")[0].split(",")]
+    nw, wm, wn, tm, tn = args[:5]
+    return wm * tm * 32, wn * tn * 32
+
+
+@settings(max_examples=300, deadline=None)
+@given(T=tokens, D=dims, F=dims)
+def test_gated_mlp_plan_covers_the_problem(T, D, F):
+    plan = gmlp.describe(T, D, F)
+    assert len(plan) == 2
+    for (name, grid, block, splits), (M, K) in zip(plan, [(F, D), (D, F)]):
+        assert grid >= 1 and splits >= 1 and block in (256, 512)
+        if name.startswith("gemv"):
+            assert T <= 8 and name.startswith("gemv_splitk_kernel<%d," % T)
+            strips = _cdiv(M, 256)
+            assert grid == strips * splits
+            assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
+        else:
+            assert T > 8
+            bmw, bn = _tile(name)
+            tiles = _cdiv(M, bmw) * _cdiv(T, bn)
+            assert grid == tiles * splits
+            if splits > 1:
+                assert name.endswith(", true>")
+                assert splits * 4 * bmw * bn * 2 * tiles <= 2 ** 31  # fp32 partials stay addressable
+    ws = gmlp.workspace_size(T, D, F)
+    assert ws >= T * F * 2  # holds H
+    assert ws % 256 == 0
+
+
+@settings(max_examples=100, deadline=None)
+@given(T=st.integers(min_value=1, max_value=8), D=dims, F=dims)
+def test_fused_plan_is_the_gemv_items(T, D, F):
+    (name, grid, block, splits), = gmlp.describe(T, D, F, "fused")
+    gemv = gmlp.describe(T, D, F, "gemv")
+    assert name == "gemv_fused_kernel<%d, false>" % T
+    assert grid == sum(g[1] for g in gemv) and splits == gemv[0][3]
+
+
+@settings(max_examples=200, deadline=None)
+@given(M=tokens, K=dims, N=dims)
+def test_softmax_matmul_plan(M, K, N):
+    plan = smm.describe(M, K, N)
+    assert plan[0][0].startswith("softmax_exp_rows_kernel<")
+    assert plan[0][1] == _cdiv(M, 4) and plan[0][2] == 256
+    r = int(plan[0][0].split("<")[1].rstrip(">"))
+    assert r in (1, 2, 4, 8, 16)
+    assert r == 16 or 512 * r >= K  # the row fits in registers unless streamed
+    assert smm.workspace_size(M, K, N) >= M * K * 2 + M * 4
+
+
+@settings(max_examples=100, deadline=None)
+@given(T=st.integers(min_value=0, max_value=20000), D=dims, F=dims)
+def test_workspace_holds_h_for_any_token_count(T, D, F):
+    # Including T = 0 (nothing to launch; sized as for one token).
+    assert gmlp.workspace_size(T, D, F) >= max(T, 1) * F * 2
+    assert smm.workspace_size(T, D, F) >= max(T, 1) * D * 2
+
+
+@settings(max_examples=200, deadline=None)
+@given(T=st.integers(min_value=-5, max_value=100), D=st.integers(min_value=-8, max_value=600),
+       F=st.integers(min_value=-8, max_value=600))
+def test_validation_agrees_with_workspace_size(T, D, F):
+    A = 0x10000000
+    rc = gmlp.library().gmlp_validate(T, D, F, A, A + (1 << 26), A + (2 << 26), A + (3 << 26),
+                                      A + (4 << 26))
+    ok_shape = T >= 0 and D > 0 and F > 0 and D % 8 == 0 and F % 8 == 0
+    assert (rc == 0) == ok_shape
+    assert (gmlp.workspace_size(T, D, F) > 0) == ok_shape
