@@ -31,6 +31,8 @@ constexpr int kNumRecords = 0x7fffffff;
 // (agent-scope) accesses on gfx950: the SC1 bit, the same policy the compiler
 // gives agent-scope atomic loads and stores.
 constexpr int kCoherent = 16;
+// Cache-policy operand for streaming (nontemporal) loads: the NT bit.
+constexpr int kNonTemporal = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base)
 {
@@ -47,6 +49,14 @@ __device__ __forceinline__ void load16_to_lds(__amdgpu_buffer_rsrc_t r, void *ld
                                               uint32_t voff, uint32_t soff = 0)
 {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, GMLP_LDS(lds_wave_base), 16, voff, soff, 0, 0);
+}
+
+// As load16_to_lds, with the nontemporal (streaming) cache policy: for data
+// that is read exactly once, so that it does not displace reused lines.
+__device__ __forceinline__ void load16_to_lds_stream(__amdgpu_buffer_rsrc_t r, void *lds_wave_base,
+                                                     uint32_t voff, uint32_t soff = 0)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, GMLP_LDS(lds_wave_base), 16, voff, soff, 0, kNonTemporal);
 }
 
 // Wait until at most n vector-memory operations of this wave are in flight

@@ -319,7 +319,11 @@ int hip_check(hipError_t e, const char *what)
 
 // ---- launches ----------------------------------------------------------------
 
-template <class S, int EPI, bool SPLIT>
+// Weights are streamed (nontemporal loads) when the plan has a single token
+// tile: then each weight element is read by one block only.
+bool stream_weights(const Step &s) { return s.tiles_n == 1; }
+
+template <class S, int EPI, bool SPLIT, bool STREAM_W = false>
 int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
                 uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, const float *rowdiv,
                 hipStream_t stream)
@@ -348,7 +352,7 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     if (s.partial_bytes > (size_t)kNumRecords)
         return fail(GMLP_ERR_UNSUPPORTED, "split-K partial sums of %zu bytes exceed the 2 GiB buffer range",
                     s.partial_bytes);
-    hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
+    hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT, STREAM_W>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
     return hip_check(hipGetLastError(), "MFMA GEMM launch");
 }
 
@@ -425,7 +429,8 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     case K_GEMM_GU_L:
         return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_S:
-        return launch_gemm<GateUpSmall, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        return stream_weights(s) ? launch_gemm<GateUpSmall, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
+                                 : launch_gemm<GateUpSmall, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);
@@ -444,8 +449,10 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
         return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
                                                          st);
     case K_GEMM_DN_S:
-        return launch_gemm<DownSmall, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
-                                                        st);
+        return stream_weights(s) ? launch_gemm<DownSmall, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                                 nullptr, rowdiv, st)
+                                 : launch_gemm<DownSmall, EPI_STORE, true, false>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                                  nullptr, rowdiv, st);
     case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);
     default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
     }
@@ -576,10 +583,12 @@ std::string shape_name()
 std::string kernel_name(const Step &s, bool gate_up)
 {
     switch (s.kind) {
-    case K_GEMM_GU_L: return "gemm_mfma_kernel<" + shape_name<GateUpLarge>() + ", 0, false>";
-    case K_GEMM_GU_S: return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true>";
-    case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false>";
-    case K_GEMM_DN_S: return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true>";
+    case K_GEMM_GU_L: return "gemm_mfma_kernel<" + shape_name<GateUpLarge>() + ", 0, false, false>";
+    case K_GEMM_GU_S:
+        return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
+    case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false, false>";
+    case K_GEMM_DN_S:
+        return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMV:
         return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
     default: return "none";

@@ -111,7 +111,13 @@ def test_describe_names_the_kernels_of_each_path(lib):
         assert block == 256 and 128 < grid <= 256 and splits > 1
     big = gmlp.describe(4096, 4096, 14336)
     assert [k[0].split("<")[0] for k in big] == ["gemm_mfma_kernel", "gemm_mfma_kernel"]
-    assert big[0][0].endswith(", 0, false>") and big[1][0].endswith(", 1, false>")
+    # <shape, epilogue, split-K, streamed weights>: prefill has neither.
+    assert big[0][0].endswith(", 0, false, false>") and big[1][0].endswith(", 1, false, false>")
+    # One token tile (T = 128): split-K, and weights read once, so streamed.
+    mid = gmlp.describe(128, 4096, 14336)
+    assert mid[0][0].endswith(", 0, true, true>") and mid[1][0].endswith(", 1, true, true>")
+    # Two token tiles re-read each weight tile: not streamed.
+    assert all(k[0].endswith(", false>") for k in gmlp.describe(256, 4096, 14336))
     assert gmlp.describe(0, 256, 512) == []
 
 
@@ -163,11 +169,11 @@ def test_variant_entry_points_validate_before_launching(lib):
 def test_softmax_matmul_describe_names_the_kernels(lib):
     big = smm.describe(8192, 8192, 8192)
     assert big[0] == ("softmax_exp_rows_kernel<16>", 2048, 256, 1)
-    assert big[1][0].startswith("gemm_mfma_kernel<GemmShape<1,") and big[1][0].endswith(", 1, false>")
+    assert big[1][0].startswith("gemm_mfma_kernel<GemmShape<1,") and big[1][0].endswith(", 1, false, false>")
     small = smm.describe(3, 4096, 1032)
     assert small[0] == ("softmax_exp_rows_kernel<8>", 1, 256, 1)
     assert small[1][0] == "gemv_splitk_kernel<3, 1, 1, false>"
-    assert smm.describe(3, 4096, 1032, "mfma")[1][0].endswith(", 1, true>")
+    assert smm.describe(3, 4096, 1032, "mfma")[1][0].endswith(", 1, true, true>")
     # Chunks per lane: the smallest power of two with 512 columns each that
     # covers K, at most 16 (longer rows are streamed).
     for K, r in [(8, 1), (512, 1), (520, 2), (1024, 2), (2048, 4), (4104, 16), (8192, 16),

@@ -43,8 +43,12 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
             bmw, bn = _tile(name)
             tiles = _cdiv(M, bmw) * _cdiv(T, bn)
             assert grid == tiles * splits
+            split_k, streamed = [f.strip() == "true" for f in name[:-1].split(">, ")[1].split(",")[1:]]
+            # Weights take the streaming cache policy exactly when one token
+            # tile reads each of them once.
+            assert streamed == (_cdiv(T, bn) == 1)
             if splits > 1:
-                assert name.endswith(", true>")
+                assert split_k
                 assert splits * 4 * bmw * bn * 2 * tiles <= 2 ** 31  # fp32 partials stay addressable
     ws = gmlp.workspace_size(T, D, F)
     assert ws >= T * F * 2  # holds H
