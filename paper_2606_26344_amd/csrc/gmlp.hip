@@ -175,8 +175,11 @@ int gemv_batch_span(int nt)
 // (gate/up 56 strips x 4 splits, down 16 x 14: 224 blocks of 1024 rows);
 // more, shorter blocks add partial sums and reduction latency, and a second
 // block on a CU does not raise its share of HBM bandwidth.
-// With more tokens the FMA work per weight byte grows: two blocks per CU.
-int gemv_block_target(int nt) { return nt <= 4 ? 256 : 512; }
+// For T = 7, 8 a load batch is only two rows (the accumulators of 8 tokens
+// take the registers), so two blocks per CU keep enough loads in flight
+// (measured: T = 5, 6 are 9% and 4% faster with one block per CU, T = 7, 8
+// 6% and 11% slower).
+int gemv_block_target(int nt) { return nt <= 6 ? 256 : 512; }
 
 void gemv_step(Step &s, int M, int N, int K, int nw)
 {
