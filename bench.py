@@ -292,7 +292,7 @@ def run_workload(name, args):
         achieved, peak, r_unit = dom_bytes / (dom_ms / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
     else:
         achieved, peak, r_unit = dom_flops / (dom_ms / 1e3) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
-    path = args.path if args.path != "auto" else ("gemv" if T <= 8 else "mfma")
+    path = args.path if args.path != "auto" else ("gemv" if plan[0][0].startswith("gemv") else "mfma")
     props = torch.cuda.get_device_properties(dev)
     result = {
         "metric": METRIC,

@@ -68,6 +68,8 @@ RAGGED = [
     (7, 256, 1032), (8, 264, 264), (9, 256, 512), (15, 264, 520), (16, 520, 1032),
     (17, 520, 1032), (33, 72, 136), (127, 256, 520), (128, 264, 1032), (129, 520, 264),
     (255, 256, 264), (257, 264, 520), (300, 1032, 2056),
+    # 32- and 64-token tiles (T <= 32, T <= 64), at their edges.
+    (32, 264, 1032), (48, 4104, 2056), (64, 520, 264), (65, 264, 520),
 ]
 
 
@@ -193,6 +195,13 @@ def test_full_size_workload(orc, name, nrows):
     w = I.WORKLOADS[name]
     rows = None if nrows is None else I.sample_rows(w.T, nrows)
     _run(w.T, w.D, w.F, seed=w.seed, rows=rows, unit_rms=w.unit_rms_rows, orc=orc)
+
+
+@pytest.mark.parametrize("T", [16, 48])
+def test_few_token_tiles_at_model_dims(orc, T):
+    # The 32- and 64-token tile configurations at the decode model's D and F
+    # (split-K over D = 4096 and F = 14336), on sampled rows.
+    _run(T, 4096, 14336, seed=60 + T, rows=I.sample_rows(T, 8), orc=orc)
 
 
 @pytest.mark.parametrize("T,D,F", [(257, 264, 12296), (300, 136, 24584), (513, 264, 12296)])

@@ -34,12 +34,13 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
     for (name, grid, block, splits), (M, K) in zip(plan, [(F, D), (D, F)]):
         assert grid >= 1 and splits >= 1 and block in (256, 512)
         if name.startswith("gemv"):
-            assert T <= 8 and name.startswith("gemv_splitk_kernel<%d," % T)
+            # The automatic path takes the GEMV kernels up to 6 tokens.
+            assert T <= 6 and name.startswith("gemv_splitk_kernel<%d," % T)
             strips = _cdiv(M, 256)
             assert grid == strips * splits
             assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
         else:
-            assert T > 8
+            assert T > 6
             bmw, bn = _tile(name)
             tiles = _cdiv(M, bmw) * _cdiv(T, bn)
             assert grid == tiles * splits
