@@ -456,7 +456,8 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     case K_GEMM_GU_T: // one token tile: always streamed
         return launch_gemm<GateUpTiny, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_M:
-        return launch_gemm<GateUpMid, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        return stream_weights(s) ? launch_gemm<GateUpMid, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
+                                 : launch_gemm<GateUpMid, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);
@@ -482,7 +483,10 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
     case K_GEMM_DN_T: // one token tile: always streamed
         return launch_gemm<DownTiny, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMM_DN_M:
-        return launch_gemm<DownMid, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
+        return stream_weights(s) ? launch_gemm<DownMid, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                               nullptr, rowdiv, st)
+                                 : launch_gemm<DownMid, EPI_STORE, true, false>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                                nullptr, rowdiv, st);
     case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);
     default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
     }
@@ -621,8 +625,10 @@ std::string kernel_name(const Step &s, bool gate_up)
         return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_T: return "gemm_mfma_kernel<" + shape_name<GateUpTiny>() + ", 0, true, true>";
     case K_GEMM_DN_T: return "gemm_mfma_kernel<" + shape_name<DownTiny>() + ", 1, true, true>";
-    case K_GEMM_GU_M: return "gemm_mfma_kernel<" + shape_name<GateUpMid>() + ", 0, true, true>";
-    case K_GEMM_DN_M: return "gemm_mfma_kernel<" + shape_name<DownMid>() + ", 1, true, true>";
+    case K_GEMM_GU_M:
+        return "gemm_mfma_kernel<" + shape_name<GateUpMid>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
+    case K_GEMM_DN_M:
+        return "gemm_mfma_kernel<" + shape_name<DownMid>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMV:
         return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
     default: return "none";
