@@ -915,7 +915,16 @@ int check_smm_args(const void *X, const void *Y, const void *Z, int64_t M, int64
     return GMLP_OK;
 }
 
-Step smm_matmul_step(int64_t M, int64_t K, int64_t N, int path) { return make_plan(M, N, K, path).down; }
+// The automatic path keeps the GEMV kernel up to 8 rows here: at the square
+// shapes of the benchmark (K = N = 8192) it beats the 32-token MFMA tiles at
+// every M <= 8 (measured: 33.0 against 34.2 us at M = 8), unlike the
+// Gated MLP's pair of steps.
+Step smm_matmul_step(int64_t M, int64_t K, int64_t N, int path)
+{
+    if (path == GMLP_PATH_AUTO)
+        path = M <= kGemvMaxTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
+    return make_plan(M, N, K, path).down;
+}
 
 // Counter block, then P [M, K] bf16 (in the H slot), the matmul's split-K
 // partial sums, and the row sums [M] fp32 (in the row-scale slot).  Sized for
