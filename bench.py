@@ -126,6 +126,10 @@ def parse_args(argv=None):
                    help="after the timed region, run plain device copies of %d MiB (a known "
                         "number of bytes) for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE"
                         % (COPY_BYTES >> 20))
+    p.add_argument("--power", type=float, default=0.0, metavar="SECONDS",
+                   help="after the measurement, run steps back to back for SECONDS while sampling "
+                        "the board's socket power and shader clocks with amd-smi (context for the "
+                        "MFMA roofline: the board's power cap sets the clock)")
     p.add_argument("--vendor-gemm", action="store_true",
                    help="also time torch.matmul (the vendor GEMM library) on the same two "
                         "matmul shapes, for context (X [T,D] x [Wg|Wu] [D,2F], H [T,F] x Wd)")
@@ -357,11 +361,88 @@ def run_workload(name, args):
         del src, dst
     if args.vendor_gemm:
         result["vendor_gemm"] = vendor_gemm(T, D, F, args, wsets[0], x, stream)
+    if args.power > 0:
+        result["power"] = power_samples(step, args.power, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, X, Wg, Wu, Wd, bound, args.cpu_seconds, variant)
     del wsets, x, y, h, ws
     torch.cuda.empty_cache()
     return result
+
+
+def parse_smi_csv(text):
+    """(socket power in W, [shader clock of every XCD in MHz]) from the CSV
+    that `amd-smi metric -p -c --csv` prints, or None if a field is missing."""
+    import csv
+    import io
+    import re
+
+    try:
+        row = next(csv.DictReader(io.StringIO(text)))
+        clocks = [float(row[k]) for k in sorted(row, key=lambda k: k or "")
+                  if re.fullmatch(r"gfx_\d+_clk", k or "")]
+        return float(row["socket_power"]), clocks
+    except (StopIteration, KeyError, ValueError, TypeError):
+        return None
+
+
+def _smi_sample():
+    """One amd-smi reading (see parse_smi_csv), or None."""
+    import subprocess
+
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-p", "-c", "--csv"], capture_output=True, text=True,
+                           timeout=10)
+    except (OSError, subprocess.SubprocessError):
+        return None
+    return parse_smi_csv(r.stdout)
+
+
+def power_samples(step, seconds, stream):
+    """Run `step` back to back for `seconds` on `stream` while another thread
+    samples amd-smi every 0.25 s (after a 0.5 s settling time)."""
+    import statistics
+    import threading
+
+    import torch
+
+    samples, done = [], threading.Event()
+
+    def sampler():
+        if done.wait(0.5):
+            return
+        while not done.is_set():
+            s_ = _smi_sample()
+            if s_ is not None:
+                samples.append(s_)
+            done.wait(0.25)
+
+    th = threading.Thread(target=sampler)
+    th.start()
+    t0 = time.time()
+    n = 0
+    with torch.cuda.stream(stream):
+        while time.time() - t0 < seconds:
+            for i in range(20):
+                step(n + i)
+            n += 20
+            torch.cuda.synchronize()
+    wall = time.time() - t0
+    done.set()
+    th.join()
+    if not samples:
+        return {"error": "amd-smi gave no socket power / clock readings"}
+    watts = [s_[0] for s_ in samples]
+    clocks = [c for s_ in samples for c in s_[1]]
+    return {
+        "tool": "amd-smi metric -p -c",
+        "samples": len(samples),
+        "steps": n,
+        "us_per_step": round(wall / n * 1e6, 2),
+        "socket_power_w": {"mean": round(statistics.mean(watts), 1), "max": max(watts)},
+        "gfx_clock_mhz": {"mean": round(statistics.mean(clocks), 1), "min": min(clocks), "max": max(clocks)}
+        if clocks else None,
+    }
 
 
 def per_step_stats(fn, k, stream):

@@ -1,0 +1,25 @@
+"""bench.py --power: parsing of the board readings (no GPU, no amd-smi call)."""
+import bench
+
+HEADER = ("gpu,socket_power,gfx_voltage,soc_voltage,mem_voltage,throttle_status,power_management,"
+          + ",".join("gfx_%d_clk,gfx_%d_min_clk,gfx_%d_max_clk,gfx_%d_clk_locked,gfx_%d_deep_sleep"
+                     % ((i,) * 5) for i in range(8))
+          + ",mem_0_clk")
+
+
+def _row(power, clocks):
+    return ("0,%s,N/A,N/A,N/A,N/A,N/A," % power
+            + ",".join("%s,500,2400,DISABLED,DISABLED" % c for c in clocks) + ",2000")
+
+
+def test_parse_reads_power_and_every_xcd_clock():
+    clocks = [1646, 1567, 1692, 1609, 1728, 1639, 1666, 1604]
+    power, got = bench.parse_smi_csv(HEADER + "\n" + _row(1396, clocks) + "\n")
+    assert power == 1396.0
+    assert got == [float(c) for c in clocks]  # gfx_N_clk only, not min/max/mem clocks
+
+
+def test_parse_rejects_missing_or_unreadable_fields():
+    assert bench.parse_smi_csv("") is None
+    assert bench.parse_smi_csv("gpu,gfx_0_clk\n0,1600\n") is None      # no socket_power
+    assert bench.parse_smi_csv(HEADER + "\n" + _row("N/A", [1600] * 8)) is None
