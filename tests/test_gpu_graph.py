@@ -25,7 +25,8 @@ def _gpu():
 
 CASES = [(1, 1032, 2056, "auto", {}), (4, 1032, 2056, "fused", {}), (3, 264, 520, "gemv",
          dict(activation="swish", beta=1.702, rmsnorm=True, eps=1e-6)),
-         (200, 1032, 2056, "auto", {}), (16, 264, 520, "mfma", dict(rmsnorm=True, eps=1e-5))]
+         (200, 1032, 2056, "auto", {}), (16, 264, 520, "mfma", dict(rmsnorm=True, eps=1e-5)),
+         (48, 1032, 2056, "auto", dict(activation="sigmoid")), (7, 264, 520, "auto", {})]
 
 
 @pytest.mark.parametrize("T,D,F,path,variant", CASES, ids=["T%d-%s-%d" % (c[0], c[3], i) for i, c in enumerate(CASES)])

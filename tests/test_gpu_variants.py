@@ -43,8 +43,8 @@ def _run(orc, T, D, F, variant, seed, path="auto", rows=None, x_scale=1.0, unit_
     return _check(gmlp.to_bf16_bits(y)[rows], ref, "T=%d D=%d F=%d %s %s" % (T, D, F, variant, path))
 
 
-SHAPES = [(1, 264, 520), (3, 1032, 2056), (8, 264, 264), (17, 520, 1032), (128, 264, 1032),
-          (300, 1032, 2056)]
+SHAPES = [(1, 264, 520), (3, 1032, 2056), (8, 264, 264), (17, 520, 1032), (48, 520, 1032),
+          (128, 264, 1032), (300, 1032, 2056)]
 
 
 @pytest.mark.parametrize("name", sorted(VARIANTS))
