@@ -35,8 +35,11 @@
 // without any transpose (the operand swap the paper derives for
 // transpose(nc_matmul(a, b)), Section 4.5).
 //
-// Schedule.  One wave per SIMD holds all accumulators (up to 256 AGPRs).
-// Fragments are double-buffered in VGPRs, and the instruction order inside
+// Schedule.  A block is 4 or 8 waves (one or two per SIMD; with two, the
+// waves of a SIMD share its matrix core, so one issues MFMAs while the other
+// waits on LDS or a barrier); each wave holds its share of the tile's fp32
+// accumulators (at most 256 registers per lane with one wave per SIMD, 128
+// with two).  Fragments are double-buffered in VGPRs, and the instruction order inside
 // each k16 step is pinned with scheduling-group barriers: every MFMA is
 // followed by one LDS fragment read for the next step and, in the step that
 // follows a pipeline barrier, by one DMA issue for a future k-tile, so the
