@@ -130,6 +130,11 @@ def parse_args(argv=None):
                    help="after the measurement, run steps back to back for SECONDS while sampling "
                         "the board's socket power and shader clocks with amd-smi (context for the "
                         "MFMA roofline: the board's power cap sets the clock)")
+    p.add_argument("--sweep-tokens", metavar="T,T,...",
+                   help="instead of the benchmark line: the step time at each token count T "
+                        "(D and F of --workload, weights rotated as for the workload's decode "
+                        "shape), one JSON line per T and path; with --path auto also the GEMV "
+                        "and MFMA paths for T <= 8")
     p.add_argument("--vendor-gemm", action="store_true",
                    help="also time torch.matmul (the vendor GEMM library) on the same two "
                         "matmul shapes, for context (X [T,D] x [Wg|Wu] [D,2F], H [T,F] x Wd)")
@@ -826,6 +831,68 @@ def summarize_profile(args):
     return 0
 
 
+def sweep_tokens(name, tokens, args):
+    """Step time of the Gated MLP at each T in `tokens`, at the D and F of
+    workload `name`: K steps after W warm-up steps, HIP events on the
+    library's stream, weights rotated through enough copies to defeat the
+    256 MB Infinity Cache.  Prints one JSON line per (T, path)."""
+    import torch
+
+    from paper_2606_26344_amd import gmlp
+    from paper_2606_26344_amd import inputs as I
+
+    w = I.WORKLOADS[name]
+    D, F = w.D, w.F
+    lib = gmlp.library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    X, Wg, Wu, Wd = I.generate(max(tokens), D, F, seed=w.seed)
+    copies = args.copies or max(3, math.ceil(MALL_DEFEAT_BYTES / (2.0 * 3 * D * F)))
+    wsets = [tuple(gmlp.from_bf16_bits(a, dev) for a in (Wg, Wu, Wd))]
+    for _ in range(copies - 1):
+        wsets.append(tuple(t.clone() for t in wsets[0]))
+    xa = gmlp.from_bf16_bits(X, dev)
+    stream = torch.cuda.current_stream(dev)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    P = ctypes.c_void_p
+    wp = [tuple(P(t.data_ptr()) for t in s_) for s_ in wsets]
+    for T in tokens:
+        paths = [args.path]
+        if args.path == "auto" and T <= 8:
+            paths += ["gemv", "mfma"]
+        x = xa[:T].contiguous()
+        y = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+        ws = gmlp.Workspace(T, D, F, device=dev)
+        for path in paths:
+            path_id = gmlp._PATHS[path]
+
+            def step(i):
+                g, u, d = wp[i % copies]
+                rc = lib.gmlp_forward_ex(P(x.data_ptr()), g, u, d, P(y.data_ptr()), T, D, F, path_id,
+                                         P(ws.buffer.data_ptr()), ws.nbytes, st)
+                if rc:
+                    raise RuntimeError(gmlp.last_error())
+
+            for i in range(args.warmup):
+                step(i)
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(args.steps):
+                step(i)
+            b.record(stream)
+            b.synchronize()
+            us = a.elapsed_time(b) * 1e3 / args.steps
+            nbytes, flops = algorithmic(T, D, F)
+            print(json.dumps({
+                "T": T, "D": D, "F": F, "path": path, "us_per_step": round(us, 2),
+                "gbs": round(nbytes / us / 1e3, 1), "tflops": round(flops / us / 1e6, 1),
+                "kernels": [k for k, *_ in gmlp.describe(T, D, F, path)],
+            }), flush=True)
+        del ws, x, y
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.summarize_profile:
@@ -844,6 +911,12 @@ def main(argv=None):
         if name not in I.WORKLOADS and name not in I.SOFTMAX_MATMUL_WORKLOADS:
             print("unknown workload %r" % name, file=sys.stderr)
             return 2
+    if args.sweep_tokens:
+        if names[0] not in I.WORKLOADS:
+            print("--sweep-tokens needs a Gated MLP workload", file=sys.stderr)
+            return 2
+        sweep_tokens(names[0], [int(t) for t in args.sweep_tokens.split(",")], args)
+        return 0
     for name in names:
         run = run_softmax_matmul if name in I.SOFTMAX_MATMUL_WORKLOADS else run_workload
         print(json.dumps(run(name, args)), flush=True)
