@@ -57,13 +57,17 @@ struct GemmParams {
     const uint16_t *w1;  // [K, M] bf16 second weight (Wu) of the dual kernel
     const uint16_t *act; // [N, K] bf16, K contiguous (X, or H)
     uint16_t *out;       // [N, M] bf16 (H, or Y)
-    float *partial;      // split-K partial sums [splits][NW][N][M] fp32
+    float *partial;      // split-K partial sums, fp32, [split][tile of the launch][wave][piece][lane]
     uint32_t *counters;  // split-K arrival counter per output tile (zero on entry and exit)
     int M, N, K;
     int k_split; // K rows per split (a multiple of BK when splits > 1)
     int splits;
     int tiles_m, tiles_n;
     int group_m; // consecutive blocks sweep group_m column tiles before the next token tile
+    // This launch computes tiles [tile_base, tile_base + tile_count) of the
+    // block order of all tiles_m x tiles_n tiles (a plan can give the tiles
+    // of a last, partial round of blocks to a split-K launch of their own).
+    int tile_base, tile_count;
     // Gate/up epilogue: activation (enum Activation), swish slope, and the
     // per-token RMSNorm scales [N] (nullptr: none).
     int activation;
@@ -183,10 +187,11 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     // order; within it, consecutive blocks sweep group_m column tiles for
     // one token tile, then the next token tile, so the blocks resident on
     // one XCD share few distinct weight and activation strips in its L2.
-    const int ntiles = p.tiles_m * p.tiles_n;
+    const int ntiles = p.tile_count; // tiles of this launch
     const int id = xcd_contiguous_id(blockIdx.x, ntiles * p.splits);
     const int split = id / ntiles;
-    const int tile_id = id - split * ntiles;
+    const int local = id - split * ntiles; // tile within the launch: split-K counter and partial slot
+    const int tile_id = p.tile_base + local;
     const int per_group = p.group_m * p.tiles_n;
     const int group = tile_id / per_group;
     const int first_m = group * p.group_m;
@@ -194,7 +199,7 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     const int in_group = tile_id - group * per_group;
     const int tm = first_m + in_group % group_w;
     const int tn = in_group / group_w;
-    const int tile = tm * p.tiles_n + tn; // counter slot for split-K
+    const int tile = local;
     const int M = p.M, N = p.N, K = p.K;
     const int m0 = tm * S::BMW, n0 = tn * S::BN;
     const int kb = split * p.k_split;
@@ -444,43 +449,49 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
             return;
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        f32x4 sum[PIECES];
-        for (int sp = 0; sp < p.splits; ++sp) {
-            f32x4 x[PIECES];
-            if (sp == split) {
+        // Pieces are summed CH at a time: all of them for up to 16; the
+        // 256 x 256 tiles take four passes of 8, which keeps the loaded
+        // pieces and the sums within the register budget next to the
+        // accumulators.  Piece g = ((w * TM + mi) * TN + ni) * 4 + j holds
+        // accumulators 4j .. 4j+3 of acc[w][mi][ni].
+        constexpr int CH = PIECES > 16 ? 8 : PIECES;
+        static_assert(PIECES % CH == 0, "whole passes");
+        auto get_piece = [&](int g) __attribute__((always_inline)) {
+            const f32x16 &a = acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN];
+            const int j = g % 4;
+            return f32x4{a[4 * j], a[4 * j + 1], a[4 * j + 2], a[4 * j + 3]};
+        };
+        auto set_piece = [&](int g, const f32x4 &v) __attribute__((always_inline)) {
+            f32x16 &a = acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN];
+            const int j = g % 4;
 #pragma unroll
-                for (int w = 0; w < NW; ++w)
+            for (int e = 0; e < 4; ++e)
+                a[4 * j + e] = v[e];
+        };
 #pragma unroll
-                    for (int mi = 0; mi < TM; ++mi)
+        for (int c0 = 0; c0 < PIECES; c0 += CH) {
+            f32x4 sum[CH];
+            for (int sp = 0; sp < p.splits; ++sp) {
+                f32x4 x[CH];
+                if (sp == split) {
 #pragma unroll
-                        for (int ni = 0; ni < TN; ++ni)
+                    for (int g = 0; g < CH; ++g)
+                        x[g] = get_piece(c0 + g);
+                } else {
+                    const uint32_t base = wave_base(sp);
 #pragma unroll
-                            for (int j = 0; j < 4; ++j)
-                                x[((w * TM + mi) * TN + ni) * 4 + j] =
-                                    f32x4{acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
-                                          acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
-            } else {
-                const uint32_t base = wave_base(sp);
+                    for (int g = 0; g < CH; ++g)
+                        x[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                             prs, lane_off, base + (c0 + g) * 1024u, kCoherent));
+                }
 #pragma unroll
-                for (int g = 0; g < PIECES; ++g)
-                    x[g] = __builtin_bit_cast(
-                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, lane_off, base + g * 1024u, kCoherent));
+                for (int g = 0; g < CH; ++g)
+                    sum[g] = sp == 0 ? x[g] : sum[g] + x[g];
             }
 #pragma unroll
-            for (int g = 0; g < PIECES; ++g)
-                sum[g] = sp == 0 ? x[g] : sum[g] + x[g];
+            for (int g = 0; g < CH; ++g)
+                set_piece(c0 + g, sum[g]);
         }
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-#pragma unroll
-            for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < TN; ++ni)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            acc[w][mi][ni][4 * j + e] = sum[((w * TM + mi) * TN + ni) * 4 + j][e];
     }
 
     // ---- epilogue: fp32 -> act(r G) * (r U), or acc / d -> bf16, 8-byte row-major stores --

@@ -103,7 +103,28 @@ struct Step {
     int blocks = 0, threads = 0;
     size_t partial_bytes = 0; // fp32 split-K partial sums
     int counters = 0;         // arrival counters
+    // GEMM without split-K whose tiles leave a last round of blocks at most
+    // half full: the first tile_count tiles (whole rounds) run as planned,
+    // the last tail_tiles run in a second launch split tail_splits ways over
+    // K (tail_k_split rows each), so they fill a round instead of idling most
+    // of the chip.
+    int tile_base = 0, tile_count = 0;
+    int tail_tiles = 0, tail_splits = 1, tail_k_split = 0;
 };
+
+// The second launch of a step with a tail: its last tail_tiles tiles, split
+// over K.
+Step tail_step(const Step &s)
+{
+    Step t = s;
+    t.tile_base = s.tile_count;
+    t.tile_count = s.tail_tiles;
+    t.splits = s.tail_splits;
+    t.k_split = s.tail_k_split;
+    t.blocks = s.tail_tiles * s.tail_splits;
+    t.tail_tiles = 0;
+    return t;
+}
 
 struct Plan {
     int path = GMLP_PATH_AUTO;
@@ -123,6 +144,9 @@ struct Variant {
     bool rms = false; // RMSNorm in front
     float eps = 0.0f;
 };
+
+// Blocks of one round: one per CU of the MI355X (256 CUs).
+constexpr int kBlockTarget = 256;
 
 // Split K so that at most `target` blocks run (the small-T kernels hold one
 // block per CU: a second round of blocks would cost a whole tile's time),
@@ -151,17 +175,35 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.tiles_n = (int)cdiv(N, S::BN);
     s.group_m = std::max(1, std::min(group_m, s.tiles_m));
     const int tiles = s.tiles_m * s.tiles_n;
+    s.tile_count = tiles;
+    s.tail_tiles = 0;
+    s.tail_splits = 1;
+    s.tail_k_split = 0;
     if (allow_split)
-        choose_splits(s, tiles, 256, S::BK, 2);
+        choose_splits(s, tiles, kBlockTarget, S::BK, 2);
     else {
         s.splits = 1;
         s.k_split = K;
+        const int rem = tiles % kBlockTarget;
+        if (tiles > kBlockTarget && rem > 0 && rem <= kBlockTarget / 2) {
+            Step t = s;
+            choose_splits(t, rem, kBlockTarget, S::BK, 2);
+            if (t.splits > 1) {
+                s.tile_count = tiles - rem;
+                s.tail_tiles = rem;
+                s.tail_splits = t.splits;
+                s.tail_k_split = t.k_split;
+            }
+        }
     }
-    s.blocks = tiles * s.splits;
+    s.blocks = s.tile_count * s.splits;
     s.threads = S::NTHREADS;
-    s.counters = s.splits > 1 ? tiles : 0;
-    // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane].
-    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * tiles * S::BMW * S::BN * nw * sizeof(float) : 0;
+    s.counters = std::max(s.splits > 1 ? tiles : 0, s.tail_tiles);
+    // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane];
+    // the tail launch runs after the main one and reuses the space.
+    const size_t tile_bytes = (size_t)S::BMW * S::BN * nw * sizeof(float);
+    s.partial_bytes = std::max(s.splits > 1 ? (size_t)s.splits * tiles * tile_bytes : 0,
+                               (size_t)s.tail_splits * s.tail_tiles * tile_bytes);
 }
 
 // Rows per load batch of the 8 row groups, per token count (splits are
@@ -365,6 +407,8 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.tiles_m = s.tiles_m;
     p.tiles_n = s.tiles_n;
     p.group_m = s.group_m;
+    p.tile_base = s.tile_base;
+    p.tile_count = s.tile_count;
     p.activation = v.act;
     p.beta = v.beta;
     p.rrms = rrms;
@@ -448,8 +492,12 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
         rrms = r;
     }
     switch (s.kind) {
-    case K_GEMM_GU_L:
-        return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+    case K_GEMM_GU_L: {
+        const int rc = launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        if (rc || !s.tail_tiles)
+            return rc;
+        return launch_gemm<GateUpLarge, EPI_GATE_MUL, true>(tail_step(s), Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+    }
     case K_GEMM_GU_S:
         return stream_weights(s) ? launch_gemm<GateUpSmall, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
                                  : launch_gemm<GateUpSmall, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
@@ -472,9 +520,14 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
 {
     const Variant plain;
     switch (s.kind) {
-    case K_GEMM_DN_L:
-        return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
-                                                         st);
+    case K_GEMM_DN_L: {
+        const int rc = launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
+                                                                 st);
+        if (rc || !s.tail_tiles)
+            return rc;
+        return launch_gemm<DownLarge, EPI_STORE, true>(tail_step(s), Wd, nullptr, H, Y, ws, l, plain, nullptr,
+                                                        rowdiv, st);
+    }
     case K_GEMM_DN_S:
         return stream_weights(s) ? launch_gemm<DownSmall, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,
                                                                                  nullptr, rowdiv, st)
@@ -635,6 +688,23 @@ std::string kernel_name(const Step &s, bool gate_up)
     }
 }
 
+// The describe lines of a step: its launch, then its tail launch if any.
+std::string describe_step(const Step &s, bool gate_up)
+{
+    char tmp[200];
+    snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", kernel_name(s, gate_up).c_str(), s.blocks,
+             s.threads, s.splits);
+    std::string text = tmp;
+    if (s.tail_tiles) {
+        const Step t = tail_step(s);
+        const std::string shape = s.kind == K_GEMM_GU_L ? shape_name<GateUpLarge>() + ", 0" : shape_name<DownLarge>() + ", 1";
+        snprintf(tmp, sizeof tmp, "gemm_mfma_kernel<%s, true, false> grid=%d block=%d k_splits=%d\n", shape.c_str(),
+                 t.blocks, t.threads, t.splits);
+        text += tmp;
+    }
+    return text;
+}
+
 } // namespace
 
 extern "C" {
@@ -685,10 +755,8 @@ int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t b
         snprintf(buf, bytes, "%s", text.c_str());
         return ok();
     }
-    for (const Step *s : {&plan.gate_up, &plan.down}) {
-        const std::string name = kernel_name(*s, s == &plan.gate_up);
-        line(name.c_str(), s->blocks, s->threads, s->splits);
-    }
+    for (const Step *s : {&plan.gate_up, &plan.down})
+        text += describe_step(*s, s == &plan.gate_up);
     snprintf(buf, bytes, "%s", text.c_str());
     return ok();
 }
@@ -993,9 +1061,8 @@ int softmax_matmul_describe(int64_t M, int64_t K, int64_t N, int path, char *buf
         return ok();
     const Step s = smm_matmul_step(M, K, N, path);
     const int r = softmax_chunks_per_lane((int)K);
-    snprintf(buf, bytes, "softmax_exp_rows_kernel<%d> grid=%lld block=%d k_splits=1\n%s grid=%d block=%d k_splits=%d\n",
-             r, (long long)cdiv(M, kSoftmaxThreads / 64), kSoftmaxThreads, kernel_name(s, false).c_str(),
-             s.blocks, s.threads, s.splits);
+    snprintf(buf, bytes, "softmax_exp_rows_kernel<%d> grid=%lld block=%d k_splits=1\n%s", r,
+             (long long)cdiv(M, kSoftmaxThreads / 64), kSoftmaxThreads, describe_step(s, false).c_str());
     return ok();
 }
 

@@ -204,6 +204,24 @@ def test_few_token_tiles_at_model_dims(orc, T):
     _run(T, 4096, 14336, seed=60 + T, rows=I.sample_rows(T, 8), orc=orc)
 
 
+@pytest.mark.parametrize("T,D,F", [(640, 264, 14336), (4096, 4352, 2056)])
+def test_tail_tiles_split_over_k(orc, T, D, F):
+    # 256-token tiles that leave a last round of blocks at most half full:
+    # the whole rounds run as one launch, the remaining tiles as a second,
+    # split-K launch (T = 640: 336 gate/up tiles = 256 + 80 split 3 ways;
+    # the second shape has tails in both steps, 272 tiles each).
+    plan = gmlp.describe(T, D, F)
+    assert any(", true, false>" in k and "GemmShape<2, 4, 2, 1, 4" in k for k, *_ in plan)
+    _run(T, D, F, seed=T + F, rows=I.sample_rows(T, 48), orc=orc)
+    # Fixed-order reductions: a second call gives the same bits.
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=T + F)
+    args = [_dev(a) for a in (X, Wg, Wu, Wd)]
+    a = gmlp.forward(*args).clone()
+    b = gmlp.forward(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
 @pytest.mark.parametrize("T,D,F", [(257, 264, 12296), (300, 136, 24584), (513, 264, 12296)])
 def test_large_gate_up_tiles_above_256_tokens(orc, T, D, F):
     # Above 256 tokens the 256-token gate/up tiles are used once they nearly

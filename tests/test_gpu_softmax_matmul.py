@@ -108,6 +108,13 @@ def test_benchmark_shape_sampled_rows(sorc):
     _run(sorc, w.M, w.K, w.N, seed=w.seed, rows=rows)
 
 
+def test_matmul_tail_tiles_split_over_k(sorc):
+    # 16 x 17 = 272 tiles of 256 x 256: one round, then 16 tiles split over K.
+    M, K, N = 4096, 2056, 4352
+    assert len(smm.describe(M, K, N)) == 3
+    _run(sorc, M, K, N, seed=41, rows=I.sample_rows(M, 32))
+
+
 def test_gemv_and_mfma_paths_agree(sorc):
     X, Y = I.generate_softmax_matmul(6, 4096, 1032, seed=3)
     ref = sorc.rows(X, Y)

@@ -26,31 +26,68 @@ def _tile(name):
     return wm * tm * 32, wn * tn * 32
 
 
+def _flags(name):
+    # gemm_mfma_kernel<GemmShape<...>, epilogue, split-K, streamed weights>
+    epi, split_k, streamed = [f.strip() for f in name[:-1].split(">, ")[1].split(",")]
+    return int(epi), split_k == "true", streamed == "true"
+
+
+def _steps(plan):
+    """The plan's lines grouped by step (gate/up, then down): a GEMM step may
+    be followed by the split-K launch of its tail tiles."""
+    steps = []
+    for line in plan:
+        name = line[0]
+        if name.startswith("gemv"):
+            step = 0 if name.split(",")[1].strip() == "2" else 1
+        else:
+            step = _flags(name)[0]
+        if steps and steps[-1][0] == step:
+            steps[-1][1].append(line)
+        else:
+            steps.append((step, [line]))
+    return steps
+
+
 @settings(max_examples=300, deadline=None)
 @given(T=tokens, D=dims, F=dims)
 def test_gated_mlp_plan_covers_the_problem(T, D, F):
     plan = gmlp.describe(T, D, F)
-    assert len(plan) == 2
-    for (name, grid, block, splits), (M, K) in zip(plan, [(F, D), (D, F)]):
-        assert grid >= 1 and splits >= 1 and block in (256, 512)
+    steps = _steps(plan)
+    assert [s for s, _ in steps] == [0, 1]
+    for (_, lines), (M, K) in zip(steps, [(F, D), (D, F)]):
+        for name, grid, block, splits in lines:
+            assert grid >= 1 and splits >= 1 and block in (256, 512)
+        name, grid, block, splits = lines[0]
         if name.startswith("gemv"):
             # The automatic path takes the GEMV kernels up to 6 tokens.
+            assert len(lines) == 1
             assert T <= 6 and name.startswith("gemv_splitk_kernel<%d," % T)
             strips = _cdiv(M, 256)
             assert grid == strips * splits
             assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
-        else:
-            assert T > 6
-            bmw, bn = _tile(name)
-            tiles = _cdiv(M, bmw) * _cdiv(T, bn)
-            assert grid == tiles * splits
-            split_k, streamed = [f.strip() == "true" for f in name[:-1].split(">, ")[1].split(",")[1:]]
+            continue
+        assert T > 6
+        bmw, bn = _tile(name)
+        tiles = _cdiv(M, bmw) * _cdiv(T, bn)
+        # Every tile is computed by exactly one launch of the step.
+        assert sum(g // sp for _, g, _, sp in lines) == tiles
+        for name_i, grid_i, _, splits_i in lines:
+            assert _tile(name_i) == (bmw, bn) and grid_i % splits_i == 0
+            _, split_k, streamed = _flags(name_i)
             # Weights take the streaming cache policy exactly when one token
             # tile reads each of them once.
             assert streamed == (_cdiv(T, bn) == 1)
-            if splits > 1:
+            if splits_i > 1:
                 assert split_k
-                assert splits * 4 * bmw * bn * 2 * tiles <= 2 ** 31  # fp32 partials stay addressable
+                assert splits_i * 4 * bmw * bn * 2 * (grid_i // splits_i) <= 2 ** 31  # partials addressable
+        if len(lines) == 2:
+            # Tail launch: whole rounds of 256 blocks first, then a partial
+            # round of at most half the chip split over K.
+            (_, g0, _, s0), (_, g1, _, s1) = lines
+            assert s0 == 1 and g0 % 256 == 0 and 0 < g1 // s1 <= 128 and s1 >= 2 and g1 <= 256
+        else:
+            assert len(lines) == 1
     ws = gmlp.workspace_size(T, D, F)
     assert ws >= T * F * 2  # holds H
     assert ws % 256 == 0
@@ -74,6 +111,13 @@ def test_softmax_matmul_plan(M, K, N):
     r = int(plan[0][0].split("<")[1].rstrip(">"))
     assert r in (1, 2, 4, 8, 16)
     assert r == 16 or 512 * r >= K  # the row fits in registers unless streamed
+    mm = plan[1:]
+    if mm[0][0].startswith("gemm"):
+        # The matmul's launches (a tail launch included) cover its tiles once.
+        bmw, bn = _tile(mm[0][0])
+        assert sum(g // sp for _, g, _, sp in mm) == _cdiv(N, bmw) * _cdiv(M, bn)
+    else:
+        assert len(mm) == 1 and M <= 8
     assert smm.workspace_size(M, K, N) >= M * K * 2 + M * 4
 
 
