@@ -138,7 +138,10 @@ int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, 
 /*
  * gmlp_forward with a caller-provided workspace of `ws_bytes` >=
  * gmlp_workspace_size(T, D, F) bytes, 256-byte aligned, prepared once with
- * gmlp_workspace_init.  Allocates nothing.
+ * gmlp_workspace_init.  Allocates nothing, issues no memset and leaves the
+ * workspace's counters at zero, so a call can be captured in a HIP graph and
+ * the graph replayed (the entry points that allocate their scratch cannot:
+ * they allocate, clear and free per call).
  */
 int gmlp_forward_ws(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
                     int64_t T, int64_t D, int64_t F, void *workspace, size_t ws_bytes,
