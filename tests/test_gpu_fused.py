@@ -84,3 +84,29 @@ def test_fused_repeated_calls_on_one_workspace():
     for _ in range(3):
         _run(X2, Wg2, Wu2, Wd2, "fused", ws)
         assert np.array_equal(_run(X, Wg, Wu, Wd, "fused", ws), first)
+
+
+def test_fused_next_to_a_kernel_on_another_stream():
+    # The waits of the fused kernel are on blocks of lower index only, which
+    # the hardware dispatches first, so the kernel completes with the same
+    # bits while another stream's kernel holds part of the chip (here a
+    # prefill-sized GEMM step running concurrently, both streams at the
+    # default priority).
+    X, Wg, Wu, Wd = I.generate(3, 4096, 14336, seed=12)
+    ref = _run(X, Wg, Wu, Wd, "gemv")
+    Xb, Wgb, Wub, Wdb = I.generate(2048, 1024, 4096, seed=13)
+    big = [gmlp.from_bf16_bits(a) for a in (Xb, Wgb, Wub, Wdb)]
+    ws_big = gmlp.Workspace(2048, 1024, 4096)
+    args = [gmlp.from_bf16_bits(a) for a in (X, Wg, Wu, Wd)]
+    ws = gmlp.Workspace(3, 4096, 14336)
+    y = torch.empty((3, 4096), dtype=torch.bfloat16, device="cuda")
+    other, mine = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(5):
+        with torch.cuda.stream(other):
+            for _ in range(4):
+                gmlp.forward(*big, workspace=ws_big)
+        with torch.cuda.stream(mine):
+            gmlp.forward(*args, out=y, path="fused", workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(gmlp.to_bf16_bits(y), ref)
