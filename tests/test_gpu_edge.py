@@ -68,3 +68,31 @@ def test_nan_row_stays_in_its_row(T, path, rmsnorm):
     assert np.all(np.isnan(I.bf16_bits_to_f32(Y[bad])))
     others = np.arange(T) != bad
     assert np.array_equal(Y[others], clean[others])
+
+
+def test_concurrent_calls_on_two_streams_with_their_own_workspaces():
+    # The library keeps no device state of its own: split-K counters and
+    # partial sums live in the caller's workspace, so two streams running
+    # calls at the same time, each with its workspace, give the bits of
+    # sequential calls (split-K GEMM at T = 128 and 16, GEMV at T = 3).
+    cases = [I.generate(T, 1032, 2056, seed=70 + T) for T in (128, 16, 3)]
+    dev = [[gmlp.from_bf16_bits(a) for a in c] for c in cases]
+    ref = []
+    for args in dev:
+        ref.append(gmlp.to_bf16_bits(gmlp.forward(*args, workspace=gmlp.Workspace(args[0].shape[0], 1032, 2056))))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    wss = [[gmlp.Workspace(a[0].shape[0], 1032, 2056) for a in dev] for _ in streams]
+    outs = [[torch.empty((a[0].shape[0], 1032), dtype=torch.bfloat16, device="cuda") for a in dev]
+            for _ in streams]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for s, st in enumerate(streams):
+            with torch.cuda.stream(st):
+                for rep in range(4):
+                    for i, args in enumerate(dev):
+                        gmlp.forward(*args, out=outs[s][i], workspace=wss[s][i])
+        torch.cuda.synchronize()
+        for s in range(len(streams)):
+            for i in range(len(dev)):
+                assert np.array_equal(gmlp.to_bf16_bits(outs[s][i]), ref[i])
