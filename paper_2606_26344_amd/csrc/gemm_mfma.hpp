@@ -410,8 +410,8 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     // layout, [split][tile][wave][piece][lane], so every store instruction
     // writes 1 KB of consecutive bytes.  After they complete (vmcnt 0) the
     // block counts itself in; the last block of the tile reads each split's
-    // pieces with device-coherent loads, all pieces of a split in flight at
-    // once, and adds the splits in order 0, 1, 2, ...  No cache-wide
+    // pieces with device-coherent loads (up to 16 pieces of a split in flight
+    // at once) and adds the splits in order 0, 1, 2, ...  No cache-wide
     // write-back or invalidate is needed.
     if (SPLIT && p.splits > 1) {
         constexpr int PIECES = NW * TM * TN * 4; // 4 accumulators (16 bytes) per piece
