@@ -147,6 +147,8 @@ struct Variant {
 
 // Blocks of one round: one per CU of the MI355X (256 CUs).
 constexpr int kBlockTarget = 256;
+// Splits of a tail launch (see Step::tail_tiles).
+constexpr int kMaxTailSplits = 8;
 
 // Split K so that at most `target` blocks run (the small-T kernels hold one
 // block per CU: a second round of blocks would cost a whole tile's time),
@@ -186,8 +188,10 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
         s.k_split = K;
         const int rem = tiles % kBlockTarget;
         if (tiles > kBlockTarget && rem > 0 && rem <= kBlockTarget / 2) {
+            // At most 8 splits: the last block of a tile reads the other
+            // splits' 256 x 256 partial tiles one after another.
             Step t = s;
-            choose_splits(t, rem, kBlockTarget, S::BK, 2);
+            choose_splits(t, rem, std::min(kBlockTarget, kMaxTailSplits * rem), S::BK, 2);
             if (t.splits > 1) {
                 s.tile_count = tiles - rem;
                 s.tail_tiles = rem;
