@@ -254,3 +254,30 @@ def test_fused_path_plan_and_validation(lib):
     assert lib.softmax_matmul_ws(A, A + 64 * MB, A + 128 * MB, 4, 256, 512, 3, A + 192 * MB, m,
                                  None) == 2
     assert "fused" in gmlp.last_error()
+
+
+def test_last_error_is_kept_per_thread(lib):
+    # Two host threads fail validation for different reasons at the same
+    # time; each reads back its own detail (ctypes drops the GIL in calls).
+    import threading
+
+    start = threading.Barrier(2)
+    seen = {}
+
+    def worker(key, T, D, code, needle):
+        start.wait()
+        bad = 0
+        for _ in range(500):
+            rc = lib.gmlp_validate(T, D, 512, A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB)
+            if rc != code or needle not in gmlp.last_error():
+                bad += 1
+        seen[key] = bad
+
+    threads = [threading.Thread(target=worker, args=("shape", -1, 256, 1, "invalid shape")),
+               threading.Thread(target=worker, args=("align", 4, 12, 2, "multiples of 8"))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert seen == {"shape": 0, "align": 0}
+    assert lib.gmlp_validate(4, 256, 512, A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB) == 0
