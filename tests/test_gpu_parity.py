@@ -78,6 +78,17 @@ def test_ragged_shapes(orc, T, D, F):
     _run(T, D, F, seed=T + D + F, orc=orc)
 
 
+def test_hidden_activations_past_2_gib(orc):
+    """H [T, F] of more than 2 GiB (T = 37601, F = 28672: 2.008 GiB): tile
+    base addresses are formed in 64 bits and only offsets within a tile are
+    32-bit.  The checked rows include the last ones, which lie past 2 GiB in
+    H, and rows of the down step's split-K tail tiles."""
+    T, D, F = 37601, 4096, 28672
+    assert T * F * 2 > 2 ** 31
+    rows = np.array([0, 1, 18000, 37119, 37120, 37448, 37449, 37520, 37599, 37600])
+    _run(T, D, F, seed=11, rows=rows, orc=orc)
+
+
 def _random_shapes(n, seed):
     # Token counts over every plan (GEMV, 32/64/128-token tiles, two token
     # tiles, 256-token tiles), D and F multiples of 8 up to 2056.
