@@ -115,6 +115,16 @@ def test_matmul_tail_tiles_split_over_k(sorc):
     _run(sorc, M, K, N, seed=41, rows=I.sample_rows(M, 32))
 
 
+def test_probabilities_past_2_gib(sorc):
+    """X and P = exp(X - rowmax) of more than 2 GiB each (M = 131080,
+    K = 8192): row and tile base addresses are formed in 64 bits.  The
+    checked rows include the last ones, which lie past 2 GiB."""
+    M, K, N = 131080, 8192, 264
+    assert M * K * 2 > 2 ** 31
+    rows = np.array([0, 1, 65536, 131071, 131072, 131079])
+    _run(sorc, M, K, N, seed=43, rows=rows)
+
+
 def test_gemv_and_mfma_paths_agree(sorc):
     X, Y = I.generate_softmax_matmul(6, 4096, 1032, seed=3)
     ref = sorc.rows(X, Y)
