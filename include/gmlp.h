@@ -147,6 +147,32 @@ int gmlp_forward_ws(const void *X, const void *Wg, const void *Wu, const void *W
                     int64_t T, int64_t D, int64_t F, void *workspace, size_t ws_bytes,
                     void *stream);
 
+/*
+ * gmlp_forward for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results as gmlp_forward, bit for bit, with the workspace kept
+ * in a static device array of GMLP_NOALLOC_SCRATCH_BYTES bytes inside the
+ * library instead of memory allocated per call.  Makes no hipMalloc, hipFree
+ * or other allocating call.  The caller still owns X, the weights and Y.
+ *
+ * Every device the library runs on holds one such array until the process
+ * ends.  Its first call on a device takes the array's address and clears its
+ * counters with a small kernel on `stream`; the kernels return the counters
+ * to zero when they finish, so later calls find them zero.  All calls on one
+ * device share that device's array and it keeps the last call's contents:
+ * calls that overlap on one device (concurrent streams, host threads or
+ * replayed graphs that are not ordered with each other) race on it and give
+ * wrong results.  Order them on one stream, or use gmlp_forward_ws with a
+ * workspace per stream.
+ *
+ * GMLP_ERR_UNSUPPORTED, with nothing launched, for a shape whose workspace
+ * (gmlp_workspace_size) exceeds GMLP_NOALLOC_SCRATCH_BYTES (for example
+ * T = 4096, D = 4096, F = 14336 needs 112 MiB); otherwise as gmlp_forward.
+ */
+#define GMLP_NOALLOC_SCRATCH_BYTES (64u << 20) /* 64 MiB per device */
+int gmlp_forward_noalloc(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                         int64_t T, int64_t D, int64_t F, void *stream);
+
 /* gmlp_forward_ws with the kernel path chosen explicitly (enum gmlp_path). */
 int gmlp_forward_ex(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
                     int64_t T, int64_t D, int64_t F, int path, void *workspace,

@@ -13,6 +13,7 @@
 #include <cstdio>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "gmlp.h"
@@ -841,6 +842,79 @@ int gmlp_forward(const void *X, const void *Wg, const void *Wu, const void *Wd, 
 }
 
 } // extern "C"
+
+// ---- the entry point that allocates nothing -------------------------------------
+// gmlp_forward_noalloc keeps its workspace (counter block, H, split-K partial
+// sums) in this array.  Every device the library runs on holds its own copy
+// from the moment the library's code is loaded on it until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: only
+// the per-device address from hipGetSymbolAddress may be handed to kernels.
+static __device__ __align__(256) uint8_t scratch[GMLP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Zero n 32-bit words (the counter block of the scratch array at set-up).
+__global__ void zero_words_kernel(uint32_t *p, uint32_t n)
+{
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch_ptr[kMaxDevices]; // device address of `scratch` per device (nullptr: not set up)
+
+// The current device's copy of `scratch`.  Set-up, once per device with that
+// device current: take the array's device address and zero its counter block
+// with a kernel on `st` (ordered before the caller's kernels on that stream;
+// the kernels leave the counters at zero when they finish, so later calls
+// find them zero).
+int noalloc_scratch(hipStream_t st, uint8_t **out)
+{
+    int dev = -1, rc;
+    if ((rc = hip_check(hipGetDevice(&dev), "hipGetDevice")))
+        return rc;
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(GMLP_ERR_UNSUPPORTED, "device %d: gmlp_forward_noalloc supports devices 0..%d", dev,
+                    kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        if ((rc = hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)")))
+            return rc;
+        const uint32_t words = (uint32_t)(kCounterBytes / sizeof(uint32_t));
+        hipLaunchKernelGGL(zero_words_kernel, dim3(64), dim3(256), 0, st, static_cast<uint32_t *>(p), words);
+        if ((rc = hip_check(hipGetLastError(), "scratch counter clear launch")))
+            return rc;
+        g_scratch_ptr[dev] = static_cast<uint8_t *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return GMLP_OK;
+}
+
+} // namespace
+
+extern "C" int gmlp_forward_noalloc(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                                    int64_t T, int64_t D, int64_t F, void *stream)
+{
+    int rc;
+    if ((rc = validate(T, D, F, X, Wg, Wu, Wd, Y)))
+        return rc;
+    if (T == 0)
+        return ok();
+    const Layout l = make_layout(T, D, F);
+    if (l.total > (size_t)GMLP_NOALLOC_SCRATCH_BYTES)
+        return fail(GMLP_ERR_UNSUPPORTED,
+                    "shape T=%lld D=%lld F=%lld needs %zu bytes of scratch, more than the %zu bytes "
+                    "gmlp_forward_noalloc holds (use gmlp_forward_ws with a caller workspace)",
+                    (long long)T, (long long)D, (long long)F, l.total, (size_t)GMLP_NOALLOC_SCRATCH_BYTES);
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    uint8_t *ws = nullptr;
+    if ((rc = noalloc_scratch(st, &ws)))
+        return rc;
+    return gmlp_forward_ex(X, Wg, Wu, Wd, Y, T, D, F, GMLP_PATH_AUTO, ws, (size_t)GMLP_NOALLOC_SCRATCH_BYTES,
+                           stream);
+}
 
 namespace {
 

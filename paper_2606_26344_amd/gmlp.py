@@ -53,6 +53,7 @@ _SIGNATURES = {
     "gmlp_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
     "gmlp_forward": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_forward_ws": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
+    "gmlp_forward_noalloc": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_forward_ex": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _SZ, _P],
                         ctypes.c_int),
     "gmlp_forward_variant": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _INT, _F, _INT, _F, _INT, _P,
@@ -225,6 +226,22 @@ def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tenso
         _check(lib.gmlp_forward_variant(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
                                         *_variant(activation, beta, rmsnorm, eps), _PATHS[path],
                                         _ptr(workspace.buffer), workspace.nbytes, st))
+    return out
+
+
+def forward_noalloc(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tensor,
+                    out: torch.Tensor, stream=None) -> torch.Tensor:
+    """gmlp_forward_noalloc: Y = (silu(x wg) * (x wu)) wd into the caller's
+    ``out``, with the library's static per-device scratch array as workspace
+    (no allocation; calls that overlap on one device race on that array)."""
+    T, D = x.shape
+    F = wg.shape[1]
+    dev = x.device
+    for t, name, shape in ((x, "x", (T, D)), (wg, "wg", (D, F)), (wu, "wu", (D, F)),
+                           (wd, "wd", (F, D)), (out, "out", (T, D))):
+        _expect(t, name, shape, dev)
+    _check(library().gmlp_forward_noalloc(_ptr(x), _ptr(wg), _ptr(wu), _ptr(wd), _ptr(out), T, D, F,
+                                          _stream(stream)))
     return out
 
 
