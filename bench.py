@@ -15,8 +15,13 @@ Memory-bound workloads rotate through several device copies of the weights
 (over 1 GB in total), so that each step streams its weights from HBM rather
 than from the 256 MB Infinity Cache.
 
-Prints one JSON line per workload (the default workload is the T=1 decode
-shape) with:
+By default (--workload suite) prints ONE JSON line: the T=1 decode workload
+(the HBM half of the metric) as the line's value, and under "configs" the
+other four Gated MLP workloads measured in the same run (tiny, small_batch,
+prefill and large_prefill: the MFMA half of the metric at T >= 2048), each
+with its own step time, value, roofline and CPU baseline.  --workload NAME
+prints one line for that workload alone (all: one line per workload).
+Each record has:
   value      whole-job throughput: GB/s of algorithmic bytes 2(3DF + 2TD)
              for memory-bound shapes, TFLOP/s of 6TDF for compute-bound ones;
   roofline   the dominant kernel (the gate/up kernel; with --path fused
@@ -106,9 +111,10 @@ def parse_args(argv=None):
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", default="decode",
-                   help="decode | tiny | small_batch | prefill | large_prefill | "
-                        "softmax_matmul | softmax_matmul_tiny | all")
+    p.add_argument("--workload", default="suite",
+                   help="suite (default: the decode line, with the other four Gated MLP "
+                        "workloads as nested records) | decode | tiny | small_batch | prefill | "
+                        "large_prefill | softmax_matmul | softmax_matmul_tiny | all")
     p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
     p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused"],
@@ -214,8 +220,12 @@ def run_workload(name, args):
     t_gen = time.perf_counter() - t_gen
 
     weight_bytes = 2.0 * 3 * D * F
+    # Rotating copies keeps the weights out of the 256 MB Infinity Cache for
+    # memory-bound shapes; weights of a few MB stay in the L2 caches whatever
+    # is rotated (the tiny workload is bound by latency), so they get one copy.
+    big = weight_bytes >= 64e6
     copies = args.copies or (max(3, math.ceil(MALL_DEFEAT_BYTES / weight_bytes))
-                             if bound == "hbm" else 1)
+                             if bound == "hbm" and big else 1)
     x = gmlp.from_bf16_bits(X, dev)
     wsets = [tuple(gmlp.from_bf16_bits(a, dev) for a in (Wg, Wu, Wd))]
     for _ in range(copies - 1):
@@ -228,7 +238,6 @@ def run_workload(name, args):
     P = ctypes.c_void_p
     xp, yp, hp, wsp = P(x.data_ptr()), P(y.data_ptr()), P(h.data_ptr()), P(ws.buffer.data_ptr())
     wp = [tuple(P(t.data_ptr()) for t in s) for s in wsets]
-    auto = gmlp.PATH_AUTO
     path_id = gmlp._PATHS[args.path]
     variant = VARIANTS[args.variant]
     vargs = gmlp._variant(variant.get("activation", "silu"), variant.get("beta", 1.0),
@@ -241,15 +250,19 @@ def run_workload(name, args):
         return lib.gmlp_forward_variant(xp, g, u, d, yp, T, D, F, *vargs, path_id, wsp, ws.nbytes,
                                         stream_ptr)
 
+    # The steps alone run on the step's own path (the fused path has no
+    # single-step form: its steps alone are the GEMV kernels it fuses).
+    step_path = gmlp.PATH_GEMV if args.path == "fused" else path_id
+
     def gate_up_only(i):
         g, u, _ = wp[i % copies]
         if not variant:
-            return lib.gmlp_gate_up_ws(xp, g, u, hp, T, D, F, auto, wsp, ws.nbytes, st)
-        return lib.gmlp_gate_up_variant(xp, g, u, hp, T, D, F, *vargs, auto, wsp, ws.nbytes, st)
+            return lib.gmlp_gate_up_ws(xp, g, u, hp, T, D, F, step_path, wsp, ws.nbytes, st)
+        return lib.gmlp_gate_up_variant(xp, g, u, hp, T, D, F, *vargs, step_path, wsp, ws.nbytes, st)
 
     def down_only(i):
         _, _, d = wp[i % copies]
-        return lib.gmlp_down_ws(hp, d, yp, T, F, D, auto, wsp, ws.nbytes, st)
+        return lib.gmlp_down_ws(hp, d, yp, T, F, D, step_path, wsp, ws.nbytes, st)
 
     def timed(fn, k):
         """Average ms per call over k calls on the library stream (HIP events)."""
@@ -893,6 +906,46 @@ def sweep_tokens(name, tokens, args):
         del ws, x, y
 
 
+# Fields of a workload's record that the suite keeps in its nested records.
+SUITE_KEYS = ("value", "unit", "ms_per_step", "steps", "warmup", "config", "roofline", "step",
+              "cpu_baseline")
+SUITE_HEADLINE = "decode"
+
+
+def run_suite(args):
+    """The default benchmark: one JSON line whose value is the decode
+    workload's (T = 1, the configuration the HBM half of the metric is quoted
+    on), with the other four Gated MLP workloads (tiny, small_batch, prefill,
+    large_prefill: the MFMA half of the metric) measured in the same run,
+    each with its own roofline and CPU baseline, under "configs"."""
+    from paper_2606_26344_amd import inputs as I
+
+    result = run_workload(SUITE_HEADLINE, args)
+    sub = argparse.Namespace(**vars(args))
+    sub.cpu_seconds = max(2.0, args.cpu_seconds / 2)  # bounded total run time
+    # The nested records follow the paper's protocol (20 warm-ups, then 100
+    # timed runs, Section 6.1) unless more are asked for: a prefill step takes
+    # about a millisecond, and a handful of warm-up steps leaves the clock
+    # still settling under the board's power cap.
+    sub.warmup = max(args.warmup, 20)
+    sub.steps = max(args.steps, 100)
+    sub.graph = sub.copy_calibration = sub.vendor_gemm = False
+    sub.power = 0.0
+    sub.path = "auto"  # the plan each workload's shape gets
+    configs = {}
+    for name in I.WORKLOADS:
+        if name == SUITE_HEADLINE:
+            continue
+        rec = run_workload(name, sub)
+        configs[name] = {k: rec[k] for k in SUITE_KEYS if k in rec}
+        print("suite: %s %.3f %s, %.1f us per step" % (name, rec["value"], rec["unit"],
+                                                       rec["ms_per_step"] * 1e3),
+              file=sys.stderr, flush=True)
+    result["config"]["suite"] = [SUITE_HEADLINE] + list(configs)
+    result["configs"] = configs
+    return result
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.summarize_profile:
@@ -905,8 +958,11 @@ def main(argv=None):
         return 2
     from paper_2606_26344_amd import inputs as I
 
+    if args.workload == "suite" and not args.sweep_tokens:
+        print(json.dumps(run_suite(args)), flush=True)
+        return 0
     names = (list(I.WORKLOADS) + list(I.SOFTMAX_MATMUL_WORKLOADS) if args.workload == "all"
-             else [args.workload])
+             else ["decode" if args.workload == "suite" else args.workload])
     for name in names:
         if name not in I.WORKLOADS and name not in I.SOFTMAX_MATMUL_WORKLOADS:
             print("unknown workload %r" % name, file=sys.stderr)

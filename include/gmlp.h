@@ -65,7 +65,10 @@ enum gmlp_path {
     GMLP_PATH_FUSED = 3, /* the whole MLP in one GEMV kernel: the first blocks run the gate/up
                             items, the rest the down items, each waiting only for the strips
                             of H its rows read; needs T <= 8; same Y as GMLP_PATH_GEMV bit for
-                            bit.  Only for gmlp_forward_ex / gmlp_forward_variant. */
+                            bit.  Only for gmlp_forward_ex / gmlp_forward_variant.  The waits
+                            are bounded (about a second): a down block that gives up makes the
+                            strips of Y it feeds NaN and counts itself in the workspace's
+                            give-up count (gmlp_workspace_status). */
 };
 
 /*
@@ -126,6 +129,27 @@ size_t gmlp_workspace_size(int64_t T, int64_t D, int64_t F);
  * call.  A buffer that was zero-filled by other means needs no init.
  */
 int gmlp_workspace_init(void *workspace, size_t bytes, void *stream);
+
+/*
+ * Read and clear the give-up count of a workspace: the number of down blocks
+ * of GMLP_PATH_FUSED calls on it whose bounded wait for H gave up since the
+ * last read (their strips of Y were written as NaN).  0 means every fused
+ * call on the workspace completed normally.  Synchronises `stream` (the
+ * stream the calls ran on) and copies 4 bytes to the host; not for use under
+ * graph capture.  INVALID_ARG for a NULL pointer or `bytes` below the counter
+ * block.
+ */
+int gmlp_workspace_status(void *workspace, size_t bytes, void *stream, uint32_t *fused_giveups);
+
+/*
+ * Test hook, not for production use: set how many times a down block of the
+ * fused kernel polls for H before it gives up (default about a second of
+ * polls) for the calls that follow, and return the previous value.  Tests
+ * pass 0 to make the waits give up from the host, with every kernel still
+ * running to completion.  Process-wide, not thread-safe against concurrent
+ * fused calls.
+ */
+uint32_t gmlp_test_fused_spin_limit(uint32_t limit);
 
 /*
  * Y = (silu(X Wg) * (X Wu)) Wd  for X [T, D], Wg/Wu [D, F], Wd [F, D],

@@ -89,7 +89,7 @@ struct GemvShared {
 // anyway, and the last block of the strip scales G and U by
 // r = 1 / sqrt(sum(x^2) / K + eps) before the activation.
 struct NoWait {
-    __device__ void operator()() const {}
+    __device__ bool operator()() const { return true; }
 };
 
 // One work item (a strip of columns times one split of rows).  Returns
@@ -98,7 +98,9 @@ struct NoWait {
 // reads the activations with device-coherent loads (the fused kernel hands H
 // from its gate/up blocks to its down blocks through them); with CX the
 // weights of the first batches are issued before wait() and the activations
-// only after it.
+// only after it.  wait() returns whether the activations are ready; if not
+// (a bounded wait that gave up), the block's sums are replaced by NaN, so
+// every output its strip produces is NaN rather than a wrong number.
 template <int NT, int NW, int EPI, bool RMS, bool CO = false, bool CX = false, class Wait = NoWait>
 __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvShared<NT, NW> &sh,
                                           const Wait &wait = Wait{})
@@ -196,12 +198,13 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     constexpr int DEPTH = gemv_depth<NT>();
     const int nb = (nrows + RG * U - 1) / (RG * U);
     Batch ring[DEPTH];
+    bool ready = true; // block-uniform
     // Prologue: DEPTH batches (past the split if i >= nb: never accumulated).
     if constexpr (CX) {
 #pragma unroll
         for (int i = 0; i < DEPTH; ++i)
             load_w(ring[i], i);
-        wait();
+        ready = wait();
 #pragma unroll
         for (int i = 0; i < DEPTH; ++i)
             load_x(ring[i], i);
@@ -310,6 +313,12 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
         for (int t = 0; t < NT; ++t)
             v[w][t] = ((sh.red[0][w][t][tid] + sh.red[1][w][t][tid]) + sh.red[2][w][t][tid]) +
                       sh.red[3][w][t][tid];
+    if (!ready)
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                v[w][t] = __builtin_nanf("");
     float ss[NT]; // RMS: the block's (then the whole row's) sum of x^2 per token
     if constexpr (RMS)
 #pragma unroll
@@ -445,14 +454,19 @@ void gemv_splitk_kernel(GemvParams p)
 
 struct GemvFusedParams {
     GemvParams gate_up, down;    // down.counters must not overlap gate_up.counters
-    uint32_t *ready;             // per down split s: [kFlagStride*s] gate/up strips done that
-                                 // it needs, [kFlagStride*s + 1] down blocks past the wait
-                                 // (both zero on entry and exit)
+    uint32_t *ready;             // per down split s, word [kFlagStride*s] (zero on entry and exit):
+                                 // gate/up strips done that it reads, plus kConsumerUnit per down
+                                 // block of the split past its wait
+    uint32_t *errors;            // count of down blocks whose wait gave up (sticky: the host clears it)
     uint32_t spin_limit;         // polls before a waiting block gives up
 };
 
 constexpr int kFusedMaxSplits = 512;
 constexpr int kFlagStride = 32; // words between the ready words of two splits: one 128-byte line each
+// What a down block adds to its split's ready word once past its wait; the
+// gate/up strips a split reads (at most kMaxDim / 256 = 16384) stay in the
+// low 16 bits, and down blocks per split (as many) times this unit below 2^31.
+constexpr uint32_t kConsumerUnit = 1u << 16;
 
 // Gate/up strips (of 8 * strip_lanes columns of H) that overlap the rows
 // [s * k_split, (s + 1) * k_split) of down split s.
@@ -463,31 +477,50 @@ __device__ __forceinline__ uint32_t fused_strips_of_split(const GemvParams &gu, 
     return (uint32_t)((r1 - 1) / width - r0 / width + 1);
 }
 
+// Add `delta` to a split's ready word; the add that completes the split's
+// events of this call (every gate/up strip it reads and every down block
+// past its wait: need + consumers * kConsumerUnit in all) resets the word
+// to zero.  Exactly one add completes it, and none follows, so the word is
+// zero when the kernel ends whatever order the adds land in.
+__device__ __forceinline__ void fused_ready_add(uint32_t *w, uint32_t delta, uint32_t complete)
+{
+    const uint32_t old = __hip_atomic_fetch_add(w, delta, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old + delta == complete)
+        __hip_atomic_store(w, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // What a down block waits for: every gate/up strip its split reads is
-// written (its count is complete).  Thread 0 polls the split's own line;
-// the last of the split's down blocks to get past resets the words.  Only
-// blocks of lower index (dispatched earlier) are waited for, so the wait
-// ends whatever number of blocks the device holds at once; a block that
-// polls spin_limit times goes on regardless (no wave waits for ever).
+// written (the low half of the split's ready word reaches `need`).  Thread 0
+// polls the split's own line.  Only blocks of lower index (dispatched
+// earlier) are waited for, so the wait ends whatever number of blocks the
+// device holds at once; a block that polls spin_limit times gives up: it
+// counts itself in `errors` and its sums become NaN (gemv_item), so the
+// strips of Y it feeds are NaN, never silently wrong.  Either way it adds
+// its kConsumerUnit, so the word still returns to zero.
 struct FusedWait {
-    uint32_t *w;         // the split's ready words
+    uint32_t *w;         // the split's ready word
     uint32_t need;       // gate/up strips the split reads
     uint32_t consumers;  // down blocks of the split (its strips of Y)
     uint32_t spin_limit;
-    __device__ void operator()() const
+    uint32_t *errors;
+    __device__ bool operator()() const
     {
+        __shared__ int s_ready;
         if (threadIdx.x == 0) {
-            for (uint32_t polls = 0;
-                 __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need && polls < spin_limit;
-                 ++polls)
+            uint32_t v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (uint32_t polls = 0; (v & (kConsumerUnit - 1)) < need && polls < spin_limit; ++polls) {
                 __builtin_amdgcn_s_sleep(2);
-            const uint32_t past = __hip_atomic_fetch_add(w + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (past == consumers - 1) {
-                __hip_atomic_store(w, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(w + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            const bool ready = (v & (kConsumerUnit - 1)) >= need;
+            fused_ready_add(w, kConsumerUnit, need + consumers * kConsumerUnit);
+            if (!ready)
+                __hip_atomic_fetch_add(errors, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_ready = ready;
         }
+        wait_lgkm0(); // thread 0's LDS write lands before the barrier
         barrier_only();
+        return s_ready != 0;
     }
 };
 
@@ -507,6 +540,7 @@ void gemv_fused_kernel(GemvFusedParams p)
         GemvShared<NT, 1> down;
     } sh;
     const int n_gu = p.gate_up.strips * p.gate_up.splits;
+    const uint32_t consumers = (uint32_t)p.down.strips;
     const int b = blockIdx.x;
     if (b < n_gu) {
         if (gemv_item<NT, 2, EPI_GATE_MUL, RMS, true>(p.gate_up, b, sh.gate_up)) {
@@ -517,8 +551,8 @@ void gemv_fused_kernel(GemvFusedParams p)
                 const int j = b % p.gate_up.strips;
                 const int f0 = j * width, f1 = min(p.gate_up.M, f0 + width);
                 for (int s = f0 / p.down.k_split; s <= (f1 - 1) / p.down.k_split; ++s)
-                    __hip_atomic_fetch_add(p.ready + kFlagStride * s, 1u, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+                    fused_ready_add(p.ready + kFlagStride * s, 1u,
+                                    fused_strips_of_split(p.gate_up, p.down, s) + consumers * kConsumerUnit);
             }
         }
         return;
@@ -526,7 +560,7 @@ void gemv_fused_kernel(GemvFusedParams p)
     const int item = b - n_gu;
     const int split = item / p.down.strips;
     const FusedWait wait{p.ready + kFlagStride * split, fused_strips_of_split(p.gate_up, p.down, split),
-                         (uint32_t)p.down.strips, p.spin_limit};
+                         consumers, p.spin_limit, p.errors};
     gemv_item<NT, 1, EPI_STORE, false, false, true>(p.down, item, sh.down, wait);
 }
 

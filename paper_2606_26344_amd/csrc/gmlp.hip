@@ -13,6 +13,7 @@
 #include <cstdio>
 #include <cmath>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <string>
 
@@ -78,14 +79,19 @@ constexpr size_t kAlign = 256;
 // Arrival counters sit at the start of every workspace in a block of fixed
 // size (enough for any shape: at most kMaxDim / 256 GEMV strips, fewer than
 // 256 split GEMM tiles), followed by the fused kernel's ready words (one
-// 128-byte line per down split), so a zeroed workspace stays valid when it
-// is reused for another shape.  Every kernel leaves them zero.
+// 128-byte line per down split) and a line holding the fused kernel's
+// give-up count, so a zeroed workspace stays valid when it is reused for
+// another shape.  Every kernel leaves the counters and ready words zero; the
+// give-up count stays until gmlp_workspace_status reads it.
 constexpr size_t kStripCounterBytes = 64 * 1024;
 constexpr size_t kReadyBytes = (size_t)kFusedMaxSplits * kFlagStride * sizeof(uint32_t);
-constexpr size_t kCounterBytes = kStripCounterBytes + kReadyBytes;
+constexpr size_t kErrorOffset = kStripCounterBytes + kReadyBytes;
+constexpr size_t kCounterBytes = kErrorOffset + 256;
 // Polls of a ready word (each with a short sleep) before a down block of the
 // fused kernel stops waiting: about a second, far beyond any real wait.
+// gmlp_test_fused_spin_limit changes it (tests force a give-up with 0).
 constexpr uint32_t kSpinLimit = 1u << 20;
+std::atomic<uint32_t> g_spin_limit{kSpinLimit};
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -570,7 +576,8 @@ int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void 
     fp.down.counters = fp.gate_up.counters + plan.gate_up.strips;
     fp.down.partial = reinterpret_cast<float *>(ws + l.partial_off + align_up(plan.gate_up.partial_bytes));
     fp.ready = reinterpret_cast<uint32_t *>(ws + l.counters_off + kStripCounterBytes);
-    fp.spin_limit = kSpinLimit;
+    fp.errors = reinterpret_cast<uint32_t *>(ws + l.counters_off + kErrorOffset);
+    fp.spin_limit = g_spin_limit.load();
     hipLaunchKernelGGL((gemv_fused_kernel<NT, RMS>), dim3(fused_grid(plan)), dim3(kGemvThreads), 0, st, fp);
     return hip_check(hipGetLastError(), "fused kernel launch");
 }
@@ -783,6 +790,30 @@ int gmlp_workspace_init(void *workspace, size_t bytes, void *stream)
                        "hipMemsetAsync(workspace)");
     return rc ? rc : ok();
 }
+
+int gmlp_workspace_status(void *workspace, size_t bytes, void *stream, uint32_t *fused_giveups)
+{
+    int rc;
+    if (!workspace || !fused_giveups)
+        return fail(GMLP_ERR_INVALID_ARG, "workspace and fused_giveups must not be NULL");
+    if (bytes < kCounterBytes)
+        return fail(GMLP_ERR_INVALID_ARG, "a workspace of %zu bytes has no status word (%zu needed)", bytes,
+                    kCounterBytes);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    uint32_t *word = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) + kErrorOffset);
+    uint32_t host = 0;
+    if ((rc = hip_check(hipMemcpyAsync(&host, word, sizeof host, hipMemcpyDeviceToHost, st),
+                        "hipMemcpyAsync(status)")) ||
+        (rc = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize")))
+        return rc;
+    if (host && ((rc = hip_check(hipMemsetAsync(word, 0, sizeof host, st), "hipMemsetAsync(status)")) ||
+                 (rc = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize"))))
+        return rc;
+    *fused_giveups = host;
+    return ok();
+}
+
+uint32_t gmlp_test_fused_spin_limit(uint32_t limit) { return g_spin_limit.exchange(limit); }
 
 int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y, int64_t T,
                          int64_t D, int64_t F, int activation, float beta, int rmsnorm, float eps,

@@ -51,6 +51,8 @@ _SIGNATURES = {
     "gmlp_describe": ([_I64, _I64, _I64, ctypes.c_int, ctypes.c_char_p, _SZ], ctypes.c_int),
     "gmlp_workspace_size": ([_I64, _I64, _I64], _SZ),
     "gmlp_workspace_init": ([_P, _SZ, _P], ctypes.c_int),
+    "gmlp_workspace_status": ([_P, _SZ, _P, ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
+    "gmlp_test_fused_spin_limit": ([ctypes.c_uint32], ctypes.c_uint32),
     "gmlp_forward": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
     "gmlp_forward_ws": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _SZ, _P], ctypes.c_int),
     "gmlp_forward_noalloc": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P], ctypes.c_int),
@@ -134,6 +136,19 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _empty(shape, dtype, device, stream=None) -> torch.Tensor:
+    """torch.empty on the stream the library will use the memory on.  The
+    caching allocator hands a freed block to the next allocation on the
+    stream it was allocated on without waiting for other streams, so memory
+    that a call's kernels use on `stream` must be allocated on `stream`:
+    allocated on the current stream instead, it could be given out again
+    there while the kernels still write to it."""
+    if stream is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(shape, dtype=dtype, device=device)
+
+
 def _expect(t: torch.Tensor, name: str, shape, device) -> None:
     if not isinstance(t, torch.Tensor):
         raise TypeError("%s must be a torch.Tensor" % name)
@@ -176,8 +191,9 @@ class Workspace:
         n = nbytes or workspace_size(T, D, F)
         if n == 0:
             raise ValueError("invalid shape T=%d D=%d F=%d" % (T, D, F))
-        # 256 bytes of slack so the buffer can be 256-byte aligned.
-        self.storage = torch.empty(n + 256, dtype=torch.uint8, device=device or "cuda")
+        # 256 bytes of slack so the buffer can be 256-byte aligned.  Allocated
+        # on the stream the calls will run on (see _empty).
+        self.storage = _empty(n + 256, torch.uint8, device or "cuda", stream)
         off = (-self.storage.data_ptr()) % 256
         self.buffer = self.storage[off:off + n]
         self.nbytes = n
@@ -185,6 +201,20 @@ class Workspace:
 
     def fits(self, T: int, D: int, F: int) -> bool:
         return workspace_size(T, D, F) <= self.nbytes
+
+    def fused_giveups(self, stream=None) -> int:
+        """gmlp_workspace_status: read and clear the count of fused-kernel
+        down blocks whose bounded wait gave up (their strips of Y are NaN)."""
+        n = ctypes.c_uint32(0)
+        _check(library().gmlp_workspace_status(_ptr(self.buffer), self.nbytes, _stream(stream),
+                                               ctypes.byref(n)))
+        return int(n.value)
+
+
+def fused_spin_limit(limit: int) -> int:
+    """gmlp_test_fused_spin_limit (test hook): polls before a fused-kernel
+    down block gives up, for the calls that follow; returns the previous."""
+    return int(library().gmlp_test_fused_spin_limit(limit))
 
 
 def _variant(activation: str, beta: float, rmsnorm: bool, eps: float):
@@ -209,7 +239,7 @@ def forward(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor, wd: torch.Tenso
     _expect(wu, "wu", (D, F), dev)
     _expect(wd, "wd", (F, D), dev)
     if out is None:
-        out = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+        out = _empty((T, D), torch.bfloat16, dev, stream)
     _expect(out, "out", (T, D), dev)
     lib = library()
     st = _stream(stream)
@@ -257,7 +287,7 @@ def gate_up(x: torch.Tensor, wg: torch.Tensor, wu: torch.Tensor,
     _expect(wg, "wg", (D, F), dev)
     _expect(wu, "wu", (D, F), dev)
     if out is None:
-        out = torch.empty((T, F), dtype=torch.bfloat16, device=dev)
+        out = _empty((T, F), torch.bfloat16, dev, stream)
     _expect(out, "out", (T, F), dev)
     plain = activation == "silu" and not rmsnorm
     if workspace is None and path == "auto" and plain:
@@ -287,7 +317,7 @@ def down(h: torch.Tensor, wd: torch.Tensor, out: Optional[torch.Tensor] = None,
     _expect(h, "h", (T, F), dev)
     _expect(wd, "wd", (F, D), dev)
     if out is None:
-        out = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
+        out = _empty((T, D), torch.bfloat16, dev, stream)
     _expect(out, "out", (T, D), dev)
     if workspace is None and path == "auto":
         _check(library().gmlp_down(_ptr(h), _ptr(wd), _ptr(out), T, F, D, _stream(stream)))

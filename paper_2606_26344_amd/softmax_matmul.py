@@ -20,7 +20,7 @@ from typing import Optional
 
 import torch
 
-from .gmlp import _PATHS, Workspace, _check, _expect, _parse_plan, _ptr, _stream, library
+from .gmlp import _PATHS, Workspace, _check, _empty, _expect, _parse_plan, _ptr, _stream, library
 
 
 def workspace_size(M: int, K: int, N: int) -> int:
@@ -54,7 +54,7 @@ def softmax_matmul(x: torch.Tensor, y: torch.Tensor, out: Optional[torch.Tensor]
     _expect(x, "x", (M, K), dev)
     _expect(y, "y", (K, N), dev)
     if out is None:
-        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        out = _empty((M, N), torch.bfloat16, dev, stream)
     _expect(out, "out", (M, N), dev)
     st = _stream(stream)
     if workspace is None and path == "auto":
@@ -75,10 +75,10 @@ def exp_rows(x: torch.Tensor, p: Optional[torch.Tensor] = None, s: Optional[torc
     dev = x.device
     _expect(x, "x", (M, K), dev)
     if p is None:
-        p = torch.empty((M, K), dtype=torch.bfloat16, device=dev)
+        p = _empty((M, K), torch.bfloat16, dev, stream)
     _expect(p, "p", (M, K), dev)
     if s is None:
-        s = torch.empty((M,), dtype=torch.float32, device=dev)
+        s = _empty((M,), torch.float32, dev, stream)
     if s.dtype != torch.float32 or s.shape != (M,) or not s.is_contiguous() or s.device != dev:
         raise ValueError("s must be a contiguous float32 tensor of shape (%d,) on %s" % (M, dev))
     _check(library().softmax_matmul_exp_rows(_ptr(x), _ptr(p), _ptr(s), M, K, _stream(stream)))
@@ -96,7 +96,7 @@ def divide(p: torch.Tensor, s: torch.Tensor, y: torch.Tensor, out: Optional[torc
     if s.dtype != torch.float32 or s.shape != (M,) or not s.is_contiguous() or s.device != dev:
         raise ValueError("s must be a contiguous float32 tensor of shape (%d,) on %s" % (M, dev))
     if out is None:
-        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        out = _empty((M, N), torch.bfloat16, dev, stream)
     _expect(out, "out", (M, N), dev)
     if workspace is None:
         workspace = make_workspace(M, K, N, device=dev, stream=stream)

@@ -96,3 +96,29 @@ def test_concurrent_calls_on_two_streams_with_their_own_workspaces():
         for s in range(len(streams)):
             for i in range(len(dev)):
                 assert np.array_equal(gmlp.to_bf16_bits(outs[s][i]), ref[i])
+
+
+@pytest.mark.parametrize("path", ["mfma", "gemv"])
+def test_temporary_workspace_on_a_side_stream(orc, path):
+    # forward() on a stream other than the current one, without a workspace:
+    # the binding allocates the temporary workspace (and the output) on that
+    # stream, so allocations made on the current stream right after the call
+    # cannot be handed its memory while the kernels still use it.
+    T, D, F = 6, 1032, 2056
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=31)
+    args = [gmlp.from_bf16_bits(a) for a in (X, Wg, Wu, Wd)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for _ in range(4):
+        outs.append(gmlp.forward(*args, path=path, stream=s))
+        junk = torch.full((1 << 22,), 7, dtype=torch.int32, device="cuda")  # current stream
+        del junk
+    s.synchronize()
+    torch.cuda.synchronize()
+    ref = orc.gated_mlp_rows(X, Wg, Wu, Wd)
+    first = gmlp.to_bf16_bits(outs[0])
+    for y in outs:
+        assert np.array_equal(gmlp.to_bf16_bits(y), first)
+    got = I.bf16_bits_to_f32(first).astype(np.float64)
+    assert np.all(np.abs(got - ref) <= 1e-2 * (np.abs(ref) + np.sqrt(np.mean(ref ** 2))))

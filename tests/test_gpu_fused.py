@@ -110,3 +110,50 @@ def test_fused_next_to_a_kernel_on_another_stream():
             gmlp.forward(*args, out=y, path="fused", workspace=ws)
         torch.cuda.synchronize()
         assert np.array_equal(gmlp.to_bf16_bits(y), ref)
+
+
+# Counter block at the start of a workspace: GEMV strip and GEMM tile
+# counters (64 KiB), the fused kernel's ready words (64 KiB), then the line
+# with its give-up count.
+COUNTER_BLOCK_BYTES = 64 * 1024 + 64 * 1024 + 256
+
+
+def test_fused_wait_that_gives_up_poisons_y_and_recovers():
+    # A zero poll limit, set from the host, makes every down block whose
+    # strips of H are not written yet give up at once; every kernel still runs
+    # to completion.  At the decode shape the down blocks start alongside the
+    # gate/up blocks, which take tens of microseconds, so some give up.
+    T, D, F = 1, 4096, 14336
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=21)
+    ref = _run(X, Wg, Wu, Wd, "gemv")
+    ws = gmlp.Workspace(T, D, F)
+    assert ws.fused_giveups() == 0
+    prev = gmlp.fused_spin_limit(0)
+    try:
+        bad = _run(X, Wg, Wu, Wd, "fused", ws)
+    finally:
+        gmlp.fused_spin_limit(prev)
+    giveups = ws.fused_giveups()
+    nan = np.isnan(I.bf16_bits_to_f32(bad))
+    print("fused give-ups: %d blocks, %d of %d outputs NaN" % (giveups, nan.sum(), nan.size), flush=True)
+    assert giveups > 0 and nan.any()
+    # A block that gave up turns the whole 256-column strip of Y it feeds to
+    # NaN; every other strip has the two-kernel path's bits.
+    for c0 in range(0, D, 256):
+        strip = slice(c0, c0 + 256)
+        assert nan[:, strip].all() or np.array_equal(bad[:, strip], ref[:, strip]), c0
+    # Counters and ready words are back at zero; reading the give-up count
+    # cleared it.
+    assert int(torch.count_nonzero(ws.buffer[:COUNTER_BLOCK_BYTES])) == 0
+    # The next call on the same workspace is bit-exact and gives up nowhere.
+    for _ in range(2):
+        assert np.array_equal(_run(X, Wg, Wu, Wd, "fused", ws), ref)
+    assert ws.fused_giveups() == 0
+
+
+def test_fused_ready_words_return_to_zero():
+    X, Wg, Wu, Wd = I.generate(8, 2056, 1032, seed=22)
+    ws = gmlp.Workspace(8, 2056, 1032)
+    _run(X, Wg, Wu, Wd, "fused", ws)
+    assert int(torch.count_nonzero(ws.buffer[:COUNTER_BLOCK_BYTES])) == 0
+    assert ws.fused_giveups() == 0
