@@ -94,9 +94,11 @@ const char *gmlp_last_error(void);
 
 /*
  * Host-only check of the arguments of gmlp_forward: sizes (T >= 0, D > 0,
- * F > 0, D % 8 == 0, F % 8 == 0, element counts that fit in int64 and in the
- * kernels' 32-bit tile offsets), non-NULL 16-byte aligned pointers, and Y not
- * overlapping any input.  Touches no device memory and makes no HIP call.
+ * F > 0, D % 8 == 0, F % 8 == 0, D and F at most 2^22, T at most 2^24, and no
+ * tensor of more than 2^37 elements: limits that keep the kernels' offsets
+ * within a tile in 32 bits and every launch grid within range), non-NULL
+ * 16-byte aligned pointers, and Y not overlapping any input.  Touches no
+ * device memory and makes no HIP call.
  */
 int gmlp_validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg,
                   const void *Wu, const void *Wd, const void *Y);

@@ -24,8 +24,9 @@
  *
  * Layout: dense, row-major, on the current HIP device:
  *     X [M, K]     Y [K, N]     Z [M, N]
- * K and N must be multiples of 8 (at most 2^22), M at most 2^30, and every
- * pointer 16-byte aligned.  M == 0 is valid and launches nothing.
+ * K and N must be multiples of 8 (at most 2^22), M at most 2^24, no tensor
+ * may hold more than 2^37 elements, and every pointer must be 16-byte
+ * aligned.  M == 0 is valid and launches nothing.
  *
  * Ownership, streams and errors are as in gmlp.h: the caller owns every
  * buffer; calls only enqueue work on `stream` (a hipStream_t, NULL = null

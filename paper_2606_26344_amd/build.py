@@ -2,8 +2,9 @@
 
     python -m paper_2606_26344_amd.build
 
-The library is compiled for gfx950 only.  Packed fp32 instructions are
-disabled for all device code (-packed-fp32-ops).
+The library is compiled for gfx950 only, with every warning an error.
+Packed fp32 instructions are disabled for all device code
+(-packed-fp32-ops).
 """
 from __future__ import annotations
 
@@ -18,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libgmlp.so")
 SOURCES = [os.path.join(CSRC, "gmlp.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("common.hpp", "gemm_mfma.hpp", "gemv.hpp", "rmsnorm.hpp",
-                                                     "softmax.hpp")] + [
+                                                     "softmax.hpp", "tiling.hpp", "plan.hpp")] + [
     os.path.join(INCLUDE, h) for h in ("gmlp.h", "softmax_matmul.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -29,6 +30,8 @@ FLAGS = [
     "-shared",
     "-fPIC",
     "-Wall",
+    "-Wextra",
+    "-Werror",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE,
     "-I", CSRC,

@@ -27,6 +27,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "tiling.hpp"
 
 namespace gmlp {
 
@@ -61,16 +62,6 @@ struct GemvParams {
 template <int NT, int NW>
 constexpr int gemv_reduce_batch() { return NT * NW <= 4 ? 16 : 64 / (NT * NW); }
 
-constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
-constexpr int kGemvThreads = 256;
-
-// Weight rows per lane per load batch (U), and batches in flight per lane
-// (DEPTH): DEPTH*NW*U loads of 16 bytes in flight per lane, within the
-// register budget of NT tokens.
-template <int NT>
-constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : NT <= 6 ? 4 : 2; }
-template <int NT>
-constexpr int gemv_depth() { return 2; }
 
 
 // LDS of one block: per-wave column sums, per-wave sums of squares of the
@@ -461,8 +452,6 @@ struct GemvFusedParams {
     uint32_t spin_limit;         // polls before a waiting block gives up
 };
 
-constexpr int kFusedMaxSplits = 512;
-constexpr int kFlagStride = 32; // words between the ready words of two splits: one 128-byte line each
 // What a down block adds to its split's ready word once past its wait; the
 // gate/up strips a split reads (at most kMaxDim / 256 = 16384) stay in the
 // low 16 bits, and down blocks per split (as many) times this unit below 2^31.

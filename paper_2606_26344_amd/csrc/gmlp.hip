@@ -23,367 +23,17 @@
 #include "gemv.hpp"
 #include "rmsnorm.hpp"
 #include "softmax.hpp"
+#include "plan.hpp"
 
 using namespace gmlp;
 
 namespace {
 
-thread_local char g_err[512];
-
-int fail(int code, const char *fmt, ...)
-{
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(g_err, sizeof g_err, fmt, ap);
-    va_end(ap);
-    return code;
-}
-
-int ok()
-{
-    g_err[0] = '\0';
-    return GMLP_OK;
-}
-
-// ---- tile configurations -------------------------------------------------
-// The large tiles run 8 waves (two per SIMD, each with half the
-// accumulators), so one wave's MFMAs cover the other's waits for LDS reads,
-// DMA and barriers: measured 4-7% faster than 4 waves holding the whole tile
-// at T = 4096 and T = 2048 (random bf16 data; power, and so the clock, depends
-// on the data at the board's power cap).
-//                          NW WM WN TM TN STAGES BK
-using GateUpLarge = GemmShape<2, 4, 2, 1, 4, 3, 32>; // 128 F cols x 256 tokens, per weight, 8 waves
-using GateUpSmall = GemmShape<2, 4, 2, 1, 2, 3, 64>; // 128 F cols x 128 tokens, 8 waves
-using DownLarge = GemmShape<1, 4, 2, 2, 4, 2, 64>;   // 256 D cols x 256 tokens, 8 waves
-using DownSmall = GemmShape<1, 2, 2, 2, 2, 4, 64>;   // 128 D cols x 128 tokens
-// Up to 32 tokens: the same weight tiles with one 32-token tile, so the
-// activations staged per weight byte drop fourfold.
-using GateUpTiny = GemmShape<2, 4, 1, 1, 1, 4, 64>; // 128 F cols x 32 tokens, 4 waves
-using DownTiny = GemmShape<1, 4, 1, 1, 1, 6, 64>;   // 128 D cols x 32 tokens, 4 waves
-using GateUpMid = GemmShape<2, 4, 1, 1, 2, 3, 64>;  // 128 F cols x 64 tokens, 4 waves
-using DownMid = GemmShape<1, 4, 1, 1, 2, 6, 64>;    // 128 D cols x 64 tokens, 4 waves
-// Column tiles swept per token tile by consecutive blocks (L2 locality),
-// from a sweep at T=4096/2048 on MI355X.
-constexpr int kGroupGateUp = 8;
-constexpr int kGroupDown = 8;
-
-constexpr int kGemvMaxTokens = 8;
-// The automatic path takes the GEMV kernels up to this many tokens.  From 7
-// tokens the 32-token MFMA tiles are faster (measured at D = 4096,
-// F = 14336: 70.7 us against 74.6 us at T = 7 and 76.7 us at T = 8; equal at
-// T = 6), since a GEMV load batch shrinks to two rows there.
-constexpr int kGemvAutoTokens = 6;
-constexpr int64_t kMaxDim = int64_t(1) << 22; // D, F: keeps 32-bit tile offsets in range
-constexpr int64_t kMaxTokens = int64_t(1) << 30;
-constexpr size_t kAlign = 256;
-// Arrival counters sit at the start of every workspace in a block of fixed
-// size (enough for any shape: at most kMaxDim / 256 GEMV strips, fewer than
-// 256 split GEMM tiles), followed by the fused kernel's ready words (one
-// 128-byte line per down split) and a line holding the fused kernel's
-// give-up count, so a zeroed workspace stays valid when it is reused for
-// another shape.  Every kernel leaves the counters and ready words zero; the
-// give-up count stays until gmlp_workspace_status reads it.
-constexpr size_t kStripCounterBytes = 64 * 1024;
-constexpr size_t kReadyBytes = (size_t)kFusedMaxSplits * kFlagStride * sizeof(uint32_t);
-constexpr size_t kErrorOffset = kStripCounterBytes + kReadyBytes;
-constexpr size_t kCounterBytes = kErrorOffset + 256;
 // Polls of a ready word (each with a short sleep) before a down block of the
 // fused kernel stops waiting: about a second, far beyond any real wait.
 // gmlp_test_fused_spin_limit changes it (tests force a give-up with 0).
 constexpr uint32_t kSpinLimit = 1u << 20;
 std::atomic<uint32_t> g_spin_limit{kSpinLimit};
-
-size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
-enum Kind { K_NONE, K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_M, K_GEMM_GU_T, K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMV };
-
-// One matmul step (gate/up or down) of a call.
-struct Step {
-    Kind kind = K_NONE;
-    int M = 0, N = 0, K = 0;
-    int tiles_m = 0, tiles_n = 0; // GEMM
-    int group_m = 1;              // GEMM block order
-    int strips = 0;               // GEMV
-    int strip_lanes = 32;         // GEMV: 8-column lanes per row
-    int splits = 1, k_split = 0;
-    int blocks = 0, threads = 0;
-    size_t partial_bytes = 0; // fp32 split-K partial sums
-    int counters = 0;         // arrival counters
-    // GEMM without split-K whose tiles leave a last round of blocks at most
-    // half full: the first tile_count tiles (whole rounds) run as planned,
-    // the last tail_tiles run in a second launch split tail_splits ways over
-    // K (tail_k_split rows each), so they fill a round instead of idling most
-    // of the chip.
-    int tile_base = 0, tile_count = 0;
-    int tail_tiles = 0, tail_splits = 1, tail_k_split = 0;
-};
-
-// The second launch of a step with a tail: its last tail_tiles tiles, split
-// over K.
-Step tail_step(const Step &s)
-{
-    Step t = s;
-    t.tile_base = s.tile_count;
-    t.tile_count = s.tail_tiles;
-    t.splits = s.tail_splits;
-    t.k_split = s.tail_k_split;
-    t.blocks = s.tail_tiles * s.tail_splits;
-    t.tail_tiles = 0;
-    return t;
-}
-
-struct Plan {
-    int path = GMLP_PATH_AUTO;
-    Step gate_up, down;
-};
-
-
-struct Layout {
-    size_t counters_off = 0, h_off = 0, partial_off = 0, rrms_off = 0, total = 0;
-    int counters = 0; // most arrival counters any path uses for this shape
-};
-
-// Which member of the Gated MLP family a call computes.
-struct Variant {
-    int act = GMLP_ACT_SILU;
-    float beta = 1.0f;
-    bool rms = false; // RMSNorm in front
-    float eps = 0.0f;
-};
-
-// Blocks of one round: one per CU of the MI355X (256 CUs).
-constexpr int kBlockTarget = 256;
-// Splits of a tail launch (see Step::tail_tiles).
-constexpr int kMaxTailSplits = 8;
-
-// Split K so that at most `target` blocks run (the small-T kernels hold one
-// block per CU: a second round of blocks would cost a whole tile's time),
-// keeping at least `min_tiles` k-tiles of `tile_k` rows per split.  Each
-// split adds T x columns fp32 partial sums to write and read back, so the
-// count rounds down.
-void choose_splits(Step &s, int tiles, int target, int tile_k, int min_tiles)
-{
-    const int64_t ktiles = cdiv(s.K, tile_k);
-    int64_t splits = 1;
-    if (tiles < target)
-        splits = std::min<int64_t>(target / tiles, std::max<int64_t>(1, ktiles / min_tiles));
-    const int64_t per = cdiv(ktiles, splits);
-    s.k_split = (int)(per * tile_k);
-    s.splits = (int)cdiv(s.K, s.k_split);
-}
-
-template <class S>
-void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split, int group_m)
-{
-    s.kind = kind;
-    s.M = M;
-    s.N = N;
-    s.K = K;
-    s.tiles_m = (int)cdiv(M, S::BMW);
-    s.tiles_n = (int)cdiv(N, S::BN);
-    s.group_m = std::max(1, std::min(group_m, s.tiles_m));
-    const int tiles = s.tiles_m * s.tiles_n;
-    s.tile_count = tiles;
-    s.tail_tiles = 0;
-    s.tail_splits = 1;
-    s.tail_k_split = 0;
-    if (allow_split)
-        choose_splits(s, tiles, kBlockTarget, S::BK, 2);
-    else {
-        s.splits = 1;
-        s.k_split = K;
-        const int rem = tiles % kBlockTarget;
-        if (tiles > kBlockTarget && rem > 0 && rem <= kBlockTarget / 2) {
-            // At most 8 splits: the last block of a tile reads the other
-            // splits' 256 x 256 partial tiles one after another.
-            Step t = s;
-            choose_splits(t, rem, std::min(kBlockTarget, kMaxTailSplits * rem), S::BK, 2);
-            if (t.splits > 1) {
-                s.tile_count = tiles - rem;
-                s.tail_tiles = rem;
-                s.tail_splits = t.splits;
-                s.tail_k_split = t.k_split;
-            }
-        }
-    }
-    s.blocks = s.tile_count * s.splits;
-    s.threads = S::NTHREADS;
-    s.counters = std::max(s.splits > 1 ? tiles : 0, s.tail_tiles);
-    // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane];
-    // the tail launch runs after the main one and reuses the space.
-    const size_t tile_bytes = (size_t)S::BMW * S::BN * nw * sizeof(float);
-    s.partial_bytes = std::max(s.splits > 1 ? (size_t)s.splits * tiles * tile_bytes : 0,
-                               (size_t)s.tail_splits * s.tail_tiles * tile_bytes);
-}
-
-// Rows per load batch of the 8 row groups, per token count (splits are
-// whole batches).
-int gemv_batch_span(int nt)
-{
-    switch (nt) {
-    case 1: return 8 * gemv_batch_rows<1>();
-    case 2: return 8 * gemv_batch_rows<2>();
-    case 3: return 8 * gemv_batch_rows<3>();
-    case 4: return 8 * gemv_batch_rows<4>();
-    case 5: return 8 * gemv_batch_rows<5>();
-    case 6: return 8 * gemv_batch_rows<6>();
-    case 7: return 8 * gemv_batch_rows<7>();
-    default: return 8 * gemv_batch_rows<8>();
-    }
-}
-
-// GEMV decomposition: strips of 256 columns (32 lanes x 8) times k splits.
-// Measured on MI355X at D=4096, F=14336 (T=1): one block per CU at most, as
-// few splits as that allows, and splits of whole load batches are fastest
-// (gate/up 56 strips x 4 splits, down 16 x 14: 224 blocks of 1024 rows);
-// more, shorter blocks add partial sums and reduction latency, and a second
-// block on a CU does not raise its share of HBM bandwidth.
-// For T = 7, 8 a load batch is only two rows (the accumulators of 8 tokens
-// take the registers), so two blocks per CU keep enough loads in flight
-// (measured: T = 5, 6 are 9% and 4% faster with one block per CU, T = 7, 8
-// 6% and 11% slower).
-int gemv_block_target(int nt) { return nt <= 6 ? 256 : 512; }
-
-void gemv_step(Step &s, int M, int N, int K, int nw)
-{
-    s.kind = K_GEMV;
-    s.M = M;
-    s.N = N;
-    s.K = K;
-    s.threads = kGemvThreads;
-    s.strip_lanes = 32;
-    s.strips = (int)cdiv(M, 8 * s.strip_lanes);
-    const int span = gemv_batch_span(N);
-    const int64_t max_sp = std::max<int64_t>(1, std::min<int64_t>(gemv_block_target(N) / s.strips, cdiv(K, span)));
-    int64_t rows = 0;
-    for (int64_t sp = max_sp; sp >= 1 && !rows; --sp)
-        if (K % sp == 0 && (K / sp) % span == 0)
-            rows = K / sp; // equal splits of whole batches
-    if (!rows || K / rows < max_sp / 2)
-        rows = cdiv(cdiv(K, max_sp), span) * span; // nearly equal splits of whole batches
-    s.k_split = (int)rows;
-    s.splits = (int)cdiv(K, rows);
-    s.blocks = s.strips * s.splits;
-    s.counters = s.splits > 1 ? s.strips : 0;
-    // Per-split column sums, then (gate/up with RMSNorm) per-strip, per-split
-    // sums of squares of X.
-    s.partial_bytes = s.splits > 1 ? (size_t)s.splits * ((size_t)nw * N * M + (size_t)s.strips * N) * sizeof(float) : 0;
-}
-
-Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
-{
-    Plan p;
-    if (path == GMLP_PATH_AUTO)
-        path = T <= kGemvAutoTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
-    p.path = path;
-    if (path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) {
-        gemv_step(p.gate_up, (int)F, (int)T, (int)D, 2);
-        gemv_step(p.down, (int)D, (int)T, (int)F, 1);
-        return p;
-    }
-    // Gate/up: large tiles once there are enough of them to fill the chip,
-    // and above 256 tokens once they at least nearly fill it: there one
-    // round of large tiles beats the partial second round that small tiles
-    // leave (measured at D = 4096, F = 14336: T = 320, 384 11% faster,
-    // T = 512 and 1024 8%).
-    const int64_t large_tiles = cdiv(T, GateUpLarge::BN) * cdiv(F, GateUpLarge::BMW);
-    if (large_tiles >= 512 || (T > 256 && large_tiles >= 192))
-        gemm_step<GateUpLarge>(p.gate_up, K_GEMM_GU_L, (int)F, (int)T, (int)D, 2, false, kGroupGateUp);
-    else if (T <= GateUpTiny::BN)
-        gemm_step<GateUpTiny>(p.gate_up, K_GEMM_GU_T, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
-    else if (T <= GateUpMid::BN)
-        gemm_step<GateUpMid>(p.gate_up, K_GEMM_GU_M, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
-    else
-        gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
-    if (cdiv(T, DownLarge::BN) * cdiv(D, DownLarge::BMW) >= 192)
-        gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false, kGroupDown);
-    else if (T <= DownTiny::BN)
-        gemm_step<DownTiny>(p.down, K_GEMM_DN_T, (int)D, (int)T, (int)F, 1, true, kGroupDown);
-    else if (T <= DownMid::BN)
-        gemm_step<DownMid>(p.down, K_GEMM_DN_M, (int)D, (int)T, (int)F, 1, true, kGroupDown);
-    else
-        gemm_step<DownSmall>(p.down, K_GEMM_DN_S, (int)D, (int)T, (int)F, 1, true, kGroupDown);
-    return p;
-}
-
-// One layout serves every path, so a workspace sized by gmlp_workspace_size
-// fits whichever kernels run.
-Layout make_layout(int64_t T, int64_t D, int64_t F)
-{
-    // T = 0 launches nothing; its workspace is sized as for one token (the
-    // plans below need at least one token tile).
-    T = std::max<int64_t>(T, 1);
-    int counters = 0;
-    size_t partial = 0;
-    for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {
-        if (path == GMLP_PATH_GEMV && T > kGemvMaxTokens)
-            continue;
-        const Plan p = make_plan(T, D, F, path);
-        counters = std::max({counters, p.gate_up.counters, p.down.counters});
-        partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes});
-        if (path == GMLP_PATH_GEMV) // the fused kernel runs both steps at once: separate partial sums
-            partial = std::max(partial, align_up(p.gate_up.partial_bytes) + p.down.partial_bytes);
-    }
-    Layout l;
-    l.counters_off = 0;
-    l.h_off = kCounterBytes;
-    l.counters = counters;
-    l.partial_off = l.h_off + align_up((size_t)T * F * 2);
-    l.rrms_off = l.partial_off + align_up(partial);
-    l.total = l.rrms_off + align_up((size_t)T * sizeof(float));
-    return l;
-}
-
-bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
-
-bool overlaps(const void *a, size_t an, const void *b, size_t bn)
-{
-    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
-    return an && bn && x < y + bn && y < x + an;
-}
-
-int check_shape(int64_t T, int64_t D, int64_t F)
-{
-    if (T < 0 || D <= 0 || F <= 0)
-        return fail(GMLP_ERR_INVALID_ARG, "invalid shape T=%lld D=%lld F=%lld (need T >= 0, D > 0, F > 0)",
-                    (long long)T, (long long)D, (long long)F);
-    if (D % 8 || F % 8)
-        return fail(GMLP_ERR_UNSUPPORTED, "D=%lld and F=%lld must be multiples of 8", (long long)D,
-                    (long long)F);
-    if (D > kMaxDim || F > kMaxDim || T > kMaxTokens)
-        return fail(GMLP_ERR_UNSUPPORTED, "shape T=%lld D=%lld F=%lld exceeds the supported range "
-                    "(D, F <= %lld, T <= %lld)", (long long)T, (long long)D, (long long)F,
-                    (long long)kMaxDim, (long long)kMaxTokens);
-    return GMLP_OK;
-}
-
-int check_ptr(const void *p, const char *name, bool required)
-{
-    if (!p)
-        return required ? fail(GMLP_ERR_INVALID_ARG, "%s is NULL", name) : GMLP_OK;
-    if (misaligned(p))
-        return fail(GMLP_ERR_UNSUPPORTED, "%s (%p) is not 16-byte aligned", name, p);
-    return GMLP_OK;
-}
-
-int validate(int64_t T, int64_t D, int64_t F, const void *X, const void *Wg, const void *Wu,
-             const void *Wd, const void *Y)
-{
-    int rc;
-    if ((rc = check_shape(T, D, F)))
-        return rc;
-    const bool rows = T > 0;
-    if ((rc = check_ptr(X, "X", rows)) || (rc = check_ptr(Wg, "Wg", true)) ||
-        (rc = check_ptr(Wu, "Wu", true)) || (rc = check_ptr(Wd, "Wd", true)) ||
-        (rc = check_ptr(Y, "Y", rows)))
-        return rc;
-    const size_t xb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
-    if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, Wg, wb) || overlaps(Y, xb, Wu, wb) ||
-        overlaps(Y, xb, Wd, wb))
-        return fail(GMLP_ERR_INVALID_ARG, "Y overlaps an input");
-    return GMLP_OK;
-}
 
 int hip_check(hipError_t e, const char *what)
 {
@@ -394,9 +44,6 @@ int hip_check(hipError_t e, const char *what)
 
 // ---- launches ----------------------------------------------------------------
 
-// Weights are streamed (nontemporal loads) when the plan has a single token
-// tile: then each weight element is read by one block only.
-bool stream_weights(const Step &s) { return s.tiles_n == 1; }
 
 template <class S, int EPI, bool SPLIT, bool STREAM_W = false>
 int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
@@ -556,9 +203,6 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
     }
 }
 
-// The fused kernel: the gate/up items on the first blocks, the down items on
-// the rest, all in one launch.
-int fused_grid(const Plan &plan) { return plan.gate_up.blocks + plan.down.blocks; }
 
 template <int NT, bool RMS>
 int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
@@ -599,56 +243,6 @@ int launch_fused(const Plan &plan, const void *X, const void *Wg, const void *Wu
     }
 }
 
-int check_variant(int activation, float beta, int rmsnorm, float eps, Variant *v)
-{
-    if (activation != GMLP_ACT_SILU && activation != GMLP_ACT_SWISH && activation != GMLP_ACT_SIGMOID)
-        return fail(GMLP_ERR_INVALID_ARG, "unknown activation %d", activation);
-    if (!std::isfinite(beta))
-        return fail(GMLP_ERR_INVALID_ARG, "beta must be finite");
-    if (rmsnorm != 0 && rmsnorm != 1)
-        return fail(GMLP_ERR_INVALID_ARG, "rmsnorm must be 0 or 1 (got %d)", rmsnorm);
-    if (rmsnorm && !(std::isfinite(eps) && eps >= 0.0f))
-        return fail(GMLP_ERR_INVALID_ARG, "eps must be finite and >= 0");
-    v->act = activation;
-    v->beta = activation == GMLP_ACT_SWISH ? beta : 1.0f;
-    v->rms = rmsnorm != 0;
-    v->eps = rmsnorm ? eps : 0.0f;
-    return GMLP_OK;
-}
-
-int check_path(int path, int64_t T)
-{
-    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA && path != GMLP_PATH_FUSED)
-        return fail(GMLP_ERR_INVALID_ARG, "unknown path %d", path);
-    if ((path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) && T > kGemvMaxTokens)
-        return fail(GMLP_ERR_UNSUPPORTED, "%s path needs T <= %d (T=%lld)",
-                    path == GMLP_PATH_GEMV ? "GEMV" : "fused", kGemvMaxTokens, (long long)T);
-    return GMLP_OK;
-}
-
-// The entry points that run one step alone (and Softmax+MatMul) have no
-// fused form.
-int check_single_step_path(int path, int64_t T)
-{
-    if (path == GMLP_PATH_FUSED)
-        return fail(GMLP_ERR_UNSUPPORTED, "the fused path runs the whole Gated MLP only");
-    return check_path(path, T);
-}
-
-int check_workspace(void *ws, size_t ws_bytes, const Layout &l)
-{
-    if (!ws)
-        return fail(GMLP_ERR_INVALID_ARG, "workspace is NULL");
-    if (reinterpret_cast<uintptr_t>(ws) % kAlign)
-        return fail(GMLP_ERR_UNSUPPORTED, "workspace %p is not %zu-byte aligned", ws, kAlign);
-    if (ws_bytes < l.total)
-        return fail(GMLP_ERR_NO_MEMORY, "workspace of %zu bytes, %zu needed", ws_bytes, l.total);
-    if ((size_t)l.counters * sizeof(uint32_t) > kStripCounterBytes)
-        return fail(GMLP_ERR_UNSUPPORTED, "shape needs %d arrival counters, more than the %zu reserved",
-                    l.counters, kCounterBytes / sizeof(uint32_t));
-    return GMLP_OK;
-}
-
 // Stream-ordered scratch for the entry points that allocate.
 struct Scratch {
     void *ptr = nullptr;
@@ -669,53 +263,6 @@ struct Scratch {
         return hip_check(hipMemsetAsync(ptr, 0, l.h_off, st), "hipMemsetAsync(counters)");
     }
 };
-
-template <class S>
-std::string shape_name()
-{
-    return "GemmShape<" + std::to_string(S::NW) + ", " + std::to_string(S::WM) + ", " +
-           std::to_string(S::WN) + ", " + std::to_string(S::TM) + ", " + std::to_string(S::TN) + ", " +
-           std::to_string(S::STAGES) + ", " + std::to_string(S::BK) + ">";
-}
-
-// A step's kernel as a profiler names it, without the namespace.
-std::string kernel_name(const Step &s, bool gate_up)
-{
-    switch (s.kind) {
-    case K_GEMM_GU_L: return "gemm_mfma_kernel<" + shape_name<GateUpLarge>() + ", 0, false, false>";
-    case K_GEMM_GU_S:
-        return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
-    case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false, false>";
-    case K_GEMM_DN_S:
-        return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
-    case K_GEMM_GU_T: return "gemm_mfma_kernel<" + shape_name<GateUpTiny>() + ", 0, true, true>";
-    case K_GEMM_DN_T: return "gemm_mfma_kernel<" + shape_name<DownTiny>() + ", 1, true, true>";
-    case K_GEMM_GU_M:
-        return "gemm_mfma_kernel<" + shape_name<GateUpMid>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
-    case K_GEMM_DN_M:
-        return "gemm_mfma_kernel<" + shape_name<DownMid>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
-    case K_GEMV:
-        return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
-    default: return "none";
-    }
-}
-
-// The describe lines of a step: its launch, then its tail launch if any.
-std::string describe_step(const Step &s, bool gate_up)
-{
-    char tmp[200];
-    snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", kernel_name(s, gate_up).c_str(), s.blocks,
-             s.threads, s.splits);
-    std::string text = tmp;
-    if (s.tail_tiles) {
-        const Step t = tail_step(s);
-        const std::string shape = s.kind == K_GEMM_GU_L ? shape_name<GateUpLarge>() + ", 0" : shape_name<DownLarge>() + ", 1";
-        snprintf(tmp, sizeof tmp, "gemm_mfma_kernel<%s, true, false> grid=%d block=%d k_splits=%d\n", shape.c_str(),
-                 t.blocks, t.threads, t.splits);
-        text += tmp;
-    }
-    return text;
-}
 
 } // namespace
 
@@ -947,36 +494,6 @@ extern "C" int gmlp_forward_noalloc(const void *X, const void *Wg, const void *W
                            stream);
 }
 
-namespace {
-
-int check_gate_up_args(const void *X, const void *Wg, const void *Wu, const void *H, int64_t T,
-                       int64_t D, int64_t F)
-{
-    int rc;
-    if ((rc = check_shape(T, D, F)) || (rc = check_ptr(X, "X", T > 0)) ||
-        (rc = check_ptr(Wg, "Wg", true)) || (rc = check_ptr(Wu, "Wu", true)) ||
-        (rc = check_ptr(H, "H", T > 0)))
-        return rc;
-    const size_t hb = (size_t)T * F * 2, xb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
-    if (overlaps(H, hb, X, xb) || overlaps(H, hb, Wg, wb) || overlaps(H, hb, Wu, wb))
-        return fail(GMLP_ERR_INVALID_ARG, "H overlaps an input");
-    return GMLP_OK;
-}
-
-int check_down_args(const void *H, const void *Wd, const void *Y, int64_t T, int64_t F, int64_t D)
-{
-    int rc;
-    if ((rc = check_shape(T, D, F)) || (rc = check_ptr(H, "H", T > 0)) ||
-        (rc = check_ptr(Wd, "Wd", true)) || (rc = check_ptr(Y, "Y", T > 0)))
-        return rc;
-    const size_t hb = (size_t)T * F * 2, yb = (size_t)T * D * 2, wb = (size_t)D * F * 2;
-    if (overlaps(Y, yb, H, hb) || overlaps(Y, yb, Wd, wb))
-        return fail(GMLP_ERR_INVALID_ARG, "Y overlaps an input");
-    return GMLP_OK;
-}
-
-} // namespace
-
 extern "C" {
 
 int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H, int64_t T, int64_t D,
@@ -1063,70 +580,6 @@ int gmlp_down(const void *H, const void *Wd, void *Y, int64_t T, int64_t F, int6
 // matmul with s as the row divisors of their epilogue.
 
 namespace {
-
-int check_smm_shape(int64_t M, int64_t K, int64_t N)
-{
-    if (M < 0 || K <= 0 || N <= 0)
-        return fail(GMLP_ERR_INVALID_ARG, "invalid shape M=%lld K=%lld N=%lld (need M >= 0, K > 0, N > 0)",
-                    (long long)M, (long long)K, (long long)N);
-    if (K % 8 || N % 8)
-        return fail(GMLP_ERR_UNSUPPORTED, "K=%lld and N=%lld must be multiples of 8", (long long)K,
-                    (long long)N);
-    if (K > kMaxDim || N > kMaxDim || M > kMaxTokens)
-        return fail(GMLP_ERR_UNSUPPORTED, "shape M=%lld K=%lld N=%lld exceeds the supported range "
-                    "(K, N <= %lld, M <= %lld)", (long long)M, (long long)K, (long long)N,
-                    (long long)kMaxDim, (long long)kMaxTokens);
-    return GMLP_OK;
-}
-
-int check_smm_args(const void *X, const void *Y, const void *Z, int64_t M, int64_t K, int64_t N)
-{
-    int rc;
-    if ((rc = check_smm_shape(M, K, N)))
-        return rc;
-    if ((rc = check_ptr(X, "X", M > 0)) || (rc = check_ptr(Y, "Y", true)) || (rc = check_ptr(Z, "Z", M > 0)))
-        return rc;
-    const size_t xb = (size_t)M * K * 2, yb = (size_t)K * N * 2, zb = (size_t)M * N * 2;
-    if (overlaps(Z, zb, X, xb) || overlaps(Z, zb, Y, yb))
-        return fail(GMLP_ERR_INVALID_ARG, "Z overlaps an input");
-    return GMLP_OK;
-}
-
-// The automatic path keeps the GEMV kernel up to 8 rows here: at the square
-// shapes of the benchmark (K = N = 8192) it beats the 32-token MFMA tiles at
-// every M <= 8 (measured: 33.0 against 34.2 us at M = 8), unlike the
-// Gated MLP's pair of steps.
-Step smm_matmul_step(int64_t M, int64_t K, int64_t N, int path)
-{
-    if (path == GMLP_PATH_AUTO)
-        path = M <= kGemvMaxTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
-    return make_plan(M, N, K, path).down;
-}
-
-// Counter block, then P [M, K] bf16 (in the H slot), the matmul's split-K
-// partial sums, and the row sums [M] fp32 (in the row-scale slot).  Sized for
-// every path of the shape.
-Layout smm_layout(int64_t M, int64_t K, int64_t N)
-{
-    M = std::max<int64_t>(M, 1); // as for make_layout: M = 0 launches nothing
-    int counters = 0;
-    size_t partial = 0;
-    for (int path : {GMLP_PATH_GEMV, GMLP_PATH_MFMA}) {
-        if (path == GMLP_PATH_GEMV && M > kGemvMaxTokens)
-            continue;
-        const Step s = smm_matmul_step(M, K, N, path);
-        counters = std::max(counters, s.counters);
-        partial = std::max(partial, s.partial_bytes);
-    }
-    Layout l;
-    l.counters_off = 0;
-    l.counters = counters;
-    l.h_off = kCounterBytes;
-    l.partial_off = l.h_off + align_up((size_t)M * K * 2);
-    l.rrms_off = l.partial_off + align_up(partial);
-    l.total = l.rrms_off + align_up((size_t)M * sizeof(float));
-    return l;
-}
 
 int launch_softmax_rows(const void *X, uint16_t *P, float *sums, int64_t M, int64_t K, hipStream_t st)
 {

@@ -1,0 +1,66 @@
+// Tile shapes and work-item constants of the Gated MLP kernels, shared by the
+// kernels (gemm_mfma.hpp, gemv.hpp) and the host-side planning (plan.hpp).
+// Plain C++: no HIP dependency.
+#pragma once
+
+namespace gmlp {
+
+// A configuration of gemm_mfma_kernel: NW weights sharing each activation
+// tile (2 for gate/up, 1 for down), a WM x WN grid of waves, each wave
+// holding TM x TN MFMA tiles of 32 x 32 outputs per weight, a ring of STAGES
+// LDS stages of BK rows of k.
+template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_, int BK_>
+struct GemmShape {
+    static constexpr int NW = NW_, WM = WM_, WN = WN_, TM = TM_, TN = TN_, STAGES = STAGES_;
+    static constexpr int BK = BK_;
+    static constexpr int KSTEPS = BK / 16;         // MFMA k16 steps per k-tile
+    static constexpr int NWAVES = WM * WN;
+    static constexpr int NTHREADS = NWAVES * 64;
+    static constexpr int BMW = WM * TM * 32;       // columns per weight per tile
+    static constexpr int BN = WN * TN * 32;        // tokens per tile
+    static constexpr int W_ROW_BYTES = BMW * 2;    // one k row of a weight tile
+    static constexpr int W_CPR = BMW / 8;          // 16-byte chunks per weight row
+    static constexpr int W_TILE_BYTES = BK * BMW * 2;
+    // Activation tiles are stored as 128-byte LDS rows of 8 chunks.  With
+    // BK = 32 one token row is 4 chunks, so row r holds token r in chunks
+    // 0..3 and token r + BN/2 in chunks 4..7.
+    static constexpr int X_HALVES = 128 / (BK * 2); // tokens per 128-byte LDS row
+    static constexpr int X_ROWS = BN / X_HALVES;    // LDS rows of an activation tile
+    static constexpr int X_CPT = BK / 8;            // 16-byte chunks per token
+    static constexpr int X_TILE_BYTES = BN * BK * 2;
+    static constexpr int STAGE_BYTES = NW * W_TILE_BYTES + X_TILE_BYTES;
+    static constexpr int W_LOADS = W_TILE_BYTES / (NTHREADS * 16); // per weight, per thread
+    static constexpr int X_LOADS = X_TILE_BYTES / (NTHREADS * 16);
+    static constexpr int LOADS_PER_STAGE = NW * W_LOADS + X_LOADS;
+    static constexpr int W_LPR = 64 / W_CPR;          // weight rows per wave load
+    static constexpr int W_RPI = NWAVES * W_LPR;      // weight rows per load step i
+    static constexpr int FRAG_READS = NW * TM * 2 + TN;  // LDS reads per k16 step
+    static constexpr int MFMAS = NW * TM * TN;           // MFMAs per k16 step
+    static_assert(BK == 32 || BK == 64, "k-tile of 32 or 64");
+    static_assert(X_ROWS % 32 == 0, "n-tiles of 32 tokens do not straddle the two row halves");
+    static_assert(BMW >= 64, "weight rows of at least 8 chunks");
+    static_assert(W_TILE_BYTES % (NTHREADS * 16) == 0 && X_TILE_BYTES % (NTHREADS * 16) == 0,
+                  "every thread issues whole 16-byte loads");
+    static_assert(STAGES >= 2 && STAGES <= 8, "2..8 LDS stages");
+    static_assert((STAGES - 2) * LOADS_PER_STAGE < 64, "vmcnt range");
+    static_assert(STAGES * STAGE_BYTES + 256 <= 160 * 1024, "LDS capacity of a CU (with the kernel's other shared words)");
+};
+
+// ---- split-K GEMV (T <= 8) ---------------------------------------------------
+constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
+constexpr int kGemvThreads = 256;
+
+// Weight rows per lane per load batch (U), and batches in flight per lane
+// (DEPTH): DEPTH*NW*U loads of 16 bytes in flight per lane, within the
+// register budget of NT tokens.
+template <int NT>
+constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : NT <= 6 ? 4 : 2; }
+template <int NT>
+constexpr int gemv_depth() { return 2; }
+
+// The fused decode kernel: at most this many down splits, each with a ready
+// word on its own 128-byte line.
+constexpr int kFusedMaxSplits = 512;
+constexpr int kFlagStride = 32; // words between the ready words of two splits: one 128-byte line each
+
+} // namespace gmlp

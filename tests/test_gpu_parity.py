@@ -99,6 +99,7 @@ def _random_shapes(n, seed):
 
 
 RANDOM = _random_shapes(16, seed=2024)
+WAIVER_CAP = 0.005  # largest fraction of elements judged against Yb only
 
 
 @pytest.mark.parametrize("T,D,F", RANDOM, ids=["T%dD%dF%d" % s for s in RANDOM])
@@ -124,8 +125,15 @@ def test_random_shapes(orc, T, D, F):
     r_b = np.abs(ref_b - ref) / bound        # the prescribed rounding alone
     r_gpu_b = np.abs(got - ref_b) / bound
     r_gpu = np.abs(got - ref) / bound
-    print("T=%d D=%d F=%d: max err/bound %.3f vs Y, %.3f vs Yb; rounding of H alone %.3f"
-          % (T, D, F, r_gpu.max(), r_gpu_b.max(), r_b.max()), flush=True)
+    waived = int(np.sum(r_b > 0.5))  # judged against Yb only (depends on the oracle alone)
+    print("T=%d D=%d F=%d: max err/bound %.3f vs Y, %.3f vs Yb; rounding of H alone %.3f; "
+          "%d of %d elements (%.3f%%) judged against Yb only"
+          % (T, D, F, r_gpu.max(), r_gpu_b.max(), r_b.max(), waived, r_b.size, 100.0 * waived / r_b.size),
+          flush=True)
+    # At these seeds the rounding of H alone passes half the bound on at most
+    # 0.23% of a shape's elements (0.04% over all sixteen shapes); the cap
+    # keeps that exemption from growing unnoticed if the shapes change.
+    assert waived <= WAIVER_CAP * r_b.size, (waived, r_b.size)
     assert np.all(r_gpu_b <= 1.0)
     assert np.all(r_gpu[r_b <= 0.5] <= 1.0)
 
@@ -280,3 +288,32 @@ def test_large_gate_up_tiles_above_256_tokens(orc, T, D, F):
     # fill the chip; ragged token tails and column tails on that path.
     assert gmlp.describe(T, D, F)[0][0].startswith("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4,")
     _run(T, D, F, seed=T + F, orc=orc)
+
+
+@pytest.mark.parametrize("T,D,F", [(1, 4096, 14336), (48, 4096, 14336), (600, 1032, 2056)])
+def test_h_is_rounded_once_to_nearest_even(orc, T, D, F):
+    """H is the fp32 value act(G) * U rounded once to bf16, to nearest even.
+    The kernel's fp32 H differs from the oracle's fp64 H by a few parts in a
+    million, so it rounds to the same bf16 as the fp64 value except near a
+    rounding boundary (expected: well under 1% of elements), and never more
+    than one bf16 step away.  The tolerance of the Y tests cannot see the
+    rounding mode (H truncated instead stays within it); truncation or a
+    second rounding would leave about half the elements one step off here."""
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=500 + T)
+    h = gmlp.gate_up(_dev(X), _dev(Wg), _dev(Wu), workspace=gmlp.Workspace(T, D, F))
+    torch.cuda.synchronize()
+    got = gmlp.to_bf16_bits(h).astype(np.int32)
+    rows = np.arange(T) if T <= 64 else I.sample_rows(T, 64)
+    _, H_ref = orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows, return_h=True)
+    want = I.f32_to_bf16_bits(H_ref.astype(np.float32)).astype(np.int32)
+    got = got[rows]
+    same = float(np.mean(got == want))
+    # Adjacent bf16 values of one sign have adjacent bit patterns.  Within a
+    # few fp32 accumulation errors of zero the sign itself is not determined,
+    # so the one-step check leaves out |H| below 1e-3 of its rms.
+    away = np.abs(H_ref) >= 1e-3 * np.sqrt(np.mean(H_ref ** 2))
+    steps = np.abs(got - want)[away]
+    print("T=%d D=%d F=%d: %.4f%% of H equal to the fp64 H rounded to nearest even, max %d step(s)"
+          % (T, D, F, 100 * same, int(steps.max())), flush=True)
+    assert same >= 0.99
+    assert steps.max() <= 1
