@@ -117,8 +117,9 @@ def parse_args(argv=None):
                         "large_prefill | softmax_matmul | softmax_matmul_tiny | all")
     p.add_argument("--variant", default="silu", choices=sorted(VARIANTS),
                    help="member of the Gated MLP family (default: the SiLU Gated MLP)")
-    p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused"],
-                   help="kernel path of the Gated MLP step (fused: both steps in one kernel, T <= 8)")
+    p.add_argument("--path", default="auto", choices=["auto", "gemv", "mfma", "fused", "fused_mfma"],
+                   help="kernel path of the Gated MLP step (fused: both GEMV steps in one kernel, "
+                        "T <= 8; fused_mfma: both MFMA steps in one kernel, T <= 64)")
     p.add_argument("--graph", action="store_true",
                    help="also time the step captured in a HIP graph (one step per weight copy, "
                         "replayed; context for launch overhead)")
@@ -139,8 +140,9 @@ def parse_args(argv=None):
     p.add_argument("--sweep-tokens", metavar="T,T,...",
                    help="instead of the benchmark line: the step time at each token count T "
                         "(D and F of --workload, weights rotated as for the workload's decode "
-                        "shape), one JSON line per T and path; with --path auto also the GEMV "
-                        "and MFMA paths for T <= 8")
+                        "shape), one JSON line per T and path; with --path auto also the GEMV, "
+                        "MFMA and fused paths for T <= 8 and the MFMA and fused MFMA paths up "
+                        "to T = 64")
     p.add_argument("--vendor-gemm", action="store_true",
                    help="also time torch.matmul (the vendor GEMM library) on the same two "
                         "matmul shapes, for context (X [T,D] x [Wg|Wu] [D,2F], H [T,F] x Wd)")
@@ -252,7 +254,7 @@ def run_workload(name, args):
 
     # The steps alone run on the step's own path (the fused path has no
     # single-step form: its steps alone are the GEMV kernels it fuses).
-    step_path = gmlp.PATH_GEMV if args.path == "fused" else path_id
+    step_path = {"fused": gmlp.PATH_GEMV, "fused_mfma": gmlp.PATH_MFMA}.get(args.path, path_id)
 
     def gate_up_only(i):
         g, u, _ = wp[i % copies]
@@ -872,7 +874,11 @@ def sweep_tokens(name, tokens, args):
     for T in tokens:
         paths = [args.path]
         if args.path == "auto" and T <= 8:
-            paths += ["gemv", "mfma"]
+            paths += ["gemv", "mfma", "fused"]
+        if args.path == "auto" and 8 < T <= 64:
+            paths += ["mfma"]
+        if args.path == "auto" and T <= 64:
+            paths += ["fused_mfma"]
         x = xa[:T].contiguous()
         y = torch.empty((T, D), dtype=torch.bfloat16, device=dev)
         ws = gmlp.Workspace(T, D, F, device=dev)

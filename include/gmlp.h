@@ -69,6 +69,12 @@ enum gmlp_path {
                             are bounded (about a second): a down block that gives up makes the
                             strips of Y it feeds NaN and counts itself in the workspace's
                             give-up count (gmlp_workspace_status). */
+    GMLP_PATH_FUSED_MFMA = 4, /* the two MFMA GEMMs of the few-token tiles in one kernel: the first
+                                 blocks run the gate/up tiles, the rest the down tiles, each down
+                                 block waiting only for the tiles of H its rows read (bounded
+                                 waits as for GMLP_PATH_FUSED); needs T <= 64; same Y as the
+                                 two-kernel GMLP_PATH_MFMA plan of the 32- and 64-token tiles, bit
+                                 for bit.  Only for gmlp_forward_ex / gmlp_forward_variant. */
 };
 
 /*
@@ -134,8 +140,9 @@ int gmlp_workspace_init(void *workspace, size_t bytes, void *stream);
 
 /*
  * Read and clear the give-up count of a workspace: the number of down blocks
- * of GMLP_PATH_FUSED calls on it whose bounded wait for H gave up since the
- * last read (their strips of Y were written as NaN).  0 means every fused
+ * of GMLP_PATH_FUSED and GMLP_PATH_FUSED_MFMA calls on it whose bounded wait
+ * for H gave up since the last read (the parts of Y they feed were written
+ * as NaN).  0 means every fused
  * call on the workspace completed normally.  Synchronises `stream` (the
  * stream the calls ran on) and copies 4 bytes to the host; not for use under
  * graph capture.  INVALID_ARG for a NULL pointer or `bytes` below the counter

@@ -121,38 +121,53 @@ __device__ __forceinline__ void interleave_step()
         __builtin_amdgcn_sched_group_barrier(kVMEMRead, N_VMEM - N_MFMA, 0);
 }
 
+// Which split and tile of a launch block `block` computes.  Each XCD gets a
+// contiguous range of the order; within it, consecutive blocks sweep
+// group_m column tiles for one token tile, then the next token tile, so the
+// blocks resident on one XCD share few distinct weight and activation strips
+// in its L2.
+__device__ __forceinline__ int gemm_split_of_block(const GemmParams &p, int block)
+{
+    return xcd_contiguous_id(block, p.tile_count * p.splits) / p.tile_count;
+}
+
+// Block-uniform wait before a block's first activation load (the fused
+// kernel's down blocks wait there for their rows of H); true when the
+// activations are ready.
+struct GemmNoWait {
+    __device__ bool operator()() const { return true; }
+};
+
+// One block's work of a GEMM launch: the output tile (or split-K piece of
+// it) of launch block `block`.  stage_ptr(std::integral_constant<int, I>)
+// gives the LDS buffer of pipeline stage I.
 // SPLIT selects the split-K variant (several blocks per output tile, summed
 // by the last one); without it p.splits must be 1.  STREAM_W loads the
 // weights with the nontemporal policy, for plans with one token tile, where
 // every weight element is read by exactly one block (measured: 5% faster at
 // T = 128, slower wherever several token tiles re-read a weight tile).
-template <class S, int EPI, bool SPLIT, bool STREAM_W>
-__global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
+// ACT_POLICY and OUT_POLICY are the cache policies of the activation loads
+// and the output stores (kCoherent where another kernel's blocks on other
+// XCDs write or read them while this kernel runs: the fused kernel's H).
+// wait() runs before the first activation load; if it returns false the
+// block's sums become NaN, so every output it feeds is NaN.  Returns the
+// first output column of the tile if this block wrote it, else -1.
+template <class S, int EPI, bool SPLIT, bool STREAM_W, int ACT_POLICY = 0, int OUT_POLICY = 0,
+          class StagePtr, class Wait = GemmNoWait>
+__device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StagePtr stage_ptr,
+                                          const Wait &wait = Wait{})
 {
+    __shared__ int s_last;
     constexpr int NW = S::NW, TM = S::TM, TN = S::TN, STAGES = S::STAGES;
     constexpr int NWAVES = S::NWAVES, KSTEPS = S::KSTEPS;
-    // One LDS array per pipeline stage: distinct objects let the compiler see
-    // that reading one stage does not depend on the DMA into another.
-    __shared__ __attribute__((aligned(1024))) uint8_t lds0[S::STAGE_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds1[S::STAGE_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds2[STAGES > 2 ? S::STAGE_BYTES : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds3[STAGES > 3 ? S::STAGE_BYTES : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds4[STAGES > 4 ? S::STAGE_BYTES : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds5[STAGES > 5 ? S::STAGE_BYTES : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds6[STAGES > 6 ? S::STAGE_BYTES : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds7[STAGES > 7 ? S::STAGE_BYTES : 16];
-    __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % S::WM, wn = wave / S::WM;
 
-    // Block -> (split, tile).  Each XCD gets a contiguous range of the
-    // order; within it, consecutive blocks sweep group_m column tiles for
-    // one token tile, then the next token tile, so the blocks resident on
-    // one XCD share few distinct weight and activation strips in its L2.
+    // Block -> (split, tile), as gemm_split_of_block.
     const int ntiles = p.tile_count; // tiles of this launch
-    const int id = xcd_contiguous_id(blockIdx.x, ntiles * p.splits);
+    const int id = xcd_contiguous_id(block, ntiles * p.splits);
     const int split = id / ntiles;
     const int local = id - split * ntiles; // tile within the launch: split-K counter and partial slot
     const int tile_id = p.tile_base + local;
@@ -170,17 +185,6 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     const int ke = min(K, kb + p.k_split);
     const int nk = (ke - kb + S::BK - 1) / S::BK;
     const bool ragged_k = (ke - kb) % S::BK != 0; // last k-tile is partial
-
-    auto stage_ptr = [&](auto s) __attribute__((always_inline)) -> uint8_t * {
-        if constexpr (decltype(s)::value == 0) return lds0;
-        else if constexpr (decltype(s)::value == 1) return lds1;
-        else if constexpr (decltype(s)::value == 2) return lds2;
-        else if constexpr (decltype(s)::value == 3) return lds3;
-        else if constexpr (decltype(s)::value == 4) return lds4;
-        else if constexpr (decltype(s)::value == 5) return lds5;
-        else if constexpr (decltype(s)::value == 6) return lds6;
-        else return lds7;
-    };
 
     // ---- staging addresses ---------------------------------------------------
     // Weight load i of this lane: row i*W_RPI + w_k, physical chunk lane %
@@ -234,7 +238,11 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
 #pragma unroll
         for (int i = 0; i < S::X_LOADS; ++i) {
             const uint32_t v = (masked && x_kcol[i] >= krem) ? kOutOfRange : x_voff[i];
-            load16_to_lds(rx, sbuf + NW * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024, v);
+            uint8_t *dst = sbuf + NW * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024;
+            if constexpr (ACT_POLICY != 0)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, GMLP_LDS(dst), 16, v, 0, 0, ACT_POLICY);
+            else
+                load16_to_lds(rx, dst, v);
         }
     };
 
@@ -320,12 +328,13 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     // the last step's MFMAs.
     static_assert(KSTEPS % 2 == 0, "k16 steps alternate between two fragment buffers");
     Frags f0, f1;
+    const bool ready = wait();
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
         (issue(stage_ptr(std::integral_constant<int, I>{}), I), ...);
     }(std::make_integer_sequence<int, STAGES - 1>{});
     wait_tile();
     issue(stage_ptr(std::integral_constant<int, STAGES - 1>{}), STAGES - 1);
-    load_frags(f0, lds0, 0);
+    load_frags(f0, stage_ptr(std::integral_constant<int, 0>{}), 0);
 
     // One k-tile held in stage buffer I, without branches: the registers
     // flow straight through (accumulators and fragments need no copies) and
@@ -367,6 +376,16 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
     // Drain the loads issued past the end before LDS can be handed to
     // another block.
     wait_vmcnt<0>();
+    if (!ready)
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        acc[w][mi][ni][e] = __builtin_nanf("");
 
     // ---- split-K: fixed-order reduction by the last block of each tile ----------
     // Each wave's partial sums go out as 16-byte device-coherent stores (sc1:
@@ -410,7 +429,7 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
         }
         __syncthreads();
         if (!s_last)
-            return;
+            return -1;
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         // Pieces are summed CH at a time: all of them for up to 16; the
@@ -519,8 +538,36 @@ __global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
                 const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
                 const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
                 const uint32_t off = n0 + tl < N && m0 + fl < M ? (uint32_t)(tl * M + fl) * 2u : kOutOfRange;
-                __builtin_amdgcn_raw_buffer_store_b64(packed[mi][ni][j], ro, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(packed[mi][ni][j], ro, off, 0, OUT_POLICY);
             }
+    return m0;
+}
+
+template <class S, int EPI, bool SPLIT, bool STREAM_W>
+__global__ __launch_bounds__(S::NTHREADS, 1) void gemm_mfma_kernel(GemmParams p)
+{
+    constexpr int STAGES = S::STAGES;
+    // One LDS array per pipeline stage: distinct objects let the compiler see
+    // that reading one stage does not depend on the DMA into another.
+    __shared__ __attribute__((aligned(1024))) uint8_t lds0[S::STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds1[S::STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds2[STAGES > 2 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds3[STAGES > 3 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds4[STAGES > 4 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds5[STAGES > 5 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds6[STAGES > 6 ? S::STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds7[STAGES > 7 ? S::STAGE_BYTES : 16];
+    auto stage_ptr = [&](auto s) __attribute__((always_inline)) -> uint8_t * {
+        if constexpr (decltype(s)::value == 0) return lds0;
+        else if constexpr (decltype(s)::value == 1) return lds1;
+        else if constexpr (decltype(s)::value == 2) return lds2;
+        else if constexpr (decltype(s)::value == 3) return lds3;
+        else if constexpr (decltype(s)::value == 4) return lds4;
+        else if constexpr (decltype(s)::value == 5) return lds5;
+        else if constexpr (decltype(s)::value == 6) return lds6;
+        else return lds7;
+    };
+    gemm_block<S, EPI, SPLIT, STREAM_W>(p, blockIdx.x, stage_ptr);
 }
 
 } // namespace gmlp

@@ -20,6 +20,7 @@
 #include "gmlp.h"
 #include "softmax_matmul.h"
 #include "gemm_mfma.hpp"
+#include "gemm_fused.hpp"
 #include "gemv.hpp"
 #include "rmsnorm.hpp"
 #include "softmax.hpp"
@@ -45,10 +46,8 @@ int hip_check(hipError_t e, const char *what)
 // ---- launches ----------------------------------------------------------------
 
 
-template <class S, int EPI, bool SPLIT, bool STREAM_W = false>
-int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
-                uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, const float *rowdiv,
-                hipStream_t stream)
+GemmParams gemm_params(const Step &s, const void *w0, const void *w1, const void *act, void *out, uint8_t *ws,
+                       const Layout &l, const Variant &v, const float *rrms, const float *rowdiv)
 {
     GemmParams p;
     p.w0 = static_cast<const uint16_t *>(w0);
@@ -71,6 +70,15 @@ int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, 
     p.beta = v.beta;
     p.rrms = rrms;
     p.rowdiv = rowdiv;
+    return p;
+}
+
+template <class S, int EPI, bool SPLIT, bool STREAM_W = false>
+int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
+                uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, const float *rowdiv,
+                hipStream_t stream)
+{
+    const GemmParams p = gemm_params(s, w0, w1, act, out, ws, l, v, rrms, rowdiv);
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
     if (s.partial_bytes > (size_t)kNumRecords)
@@ -135,19 +143,27 @@ int launch_gemv(const Step &s, const void *w0, const void *w1, const void *act, 
 
 // The gate/up step: H = bf16(act(r G) * (r U)).  With RMSNorm the GEMV
 // kernel computes r itself; the MFMA path computes r for every row first.
+// The MFMA path with RMSNorm: r = 1 / sqrt(mean(x^2) + eps) for every row of
+// X [N, K] into the workspace, for the gate/up epilogue to scale G and U by.
+int launch_row_rms(const Step &s, const void *X, uint8_t *ws, const Layout &l, const Variant &v,
+                   hipStream_t st, const float **rrms)
+{
+    float *r = reinterpret_cast<float *>(ws + l.rrms_off);
+    const int per = kRowRmsThreads / 64;
+    hipLaunchKernelGGL(row_rms_kernel, dim3((unsigned)cdiv(s.N, per)), dim3(kRowRmsThreads), 0, st,
+                       static_cast<const uint16_t *>(X), r, s.N, s.K, v.eps);
+    *rrms = r;
+    return hip_check(hipGetLastError(), "row RMS launch");
+}
+
 int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, void *H, uint8_t *ws,
                 const Layout &l, const Variant &v, hipStream_t st)
 {
     const float *rrms = nullptr;
     if (v.rms && s.kind != K_GEMV) {
-        float *r = reinterpret_cast<float *>(ws + l.rrms_off);
-        const int per = kRowRmsThreads / 64;
-        hipLaunchKernelGGL(row_rms_kernel, dim3((unsigned)cdiv(s.N, per)), dim3(kRowRmsThreads), 0, st,
-                           static_cast<const uint16_t *>(X), r, s.N, s.K, v.eps);
-        int rc = hip_check(hipGetLastError(), "row RMS launch");
+        const int rc = launch_row_rms(s, X, ws, l, v, st, &rrms);
         if (rc)
             return rc;
-        rrms = r;
     }
     switch (s.kind) {
     case K_GEMM_GU_L: {
@@ -224,6 +240,53 @@ int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void 
     fp.spin_limit = g_spin_limit.load();
     hipLaunchKernelGGL((gemv_fused_kernel<NT, RMS>), dim3(fused_grid(plan)), dim3(kGemvThreads), 0, st, fp);
     return hip_check(hipGetLastError(), "fused kernel launch");
+}
+
+// The one-launch MFMA path: gate/up tiles on the first blocks, down tiles on
+// the rest (gemm_fused.hpp).  Both steps' split-K counters and partial sums
+// are live at once: down's follow gate/up's.
+int launch_fused_mfma(const Plan &plan, const void *X, const void *Wg, const void *Wu, const void *Wd, void *Y,
+                      uint8_t *ws, const Layout &l, const Variant &v, hipStream_t st)
+{
+    const Step &gu = plan.gate_up, &dn = plan.down;
+    const bool tiny = gu.kind == K_GEMM_GU_T && dn.kind == K_GEMM_DN_T;
+    const bool mid = gu.kind == K_GEMM_GU_M && dn.kind == K_GEMM_DN_M;
+    if (!(tiny || mid) || gu.tiles_n != 1 || dn.tiles_n != 1)
+        return fail(GMLP_ERR_INVALID_ARG, "internal: fused MFMA path needs the few-token tiles");
+    if (dn.splits > kFusedMaxSplits)
+        return fail(GMLP_ERR_UNSUPPORTED, "fused MFMA path: %d down splits, at most %d", dn.splits,
+                    kFusedMaxSplits);
+    if (!fused_mfma_counters_fit(plan))
+        return fail(GMLP_ERR_UNSUPPORTED, "fused MFMA path: %d + %d tiles exceed the counter block", gu.tile_count,
+                    dn.counters);
+    if (align_up(gu.partial_bytes) + dn.partial_bytes > (size_t)kNumRecords)
+        return fail(GMLP_ERR_UNSUPPORTED, "fused MFMA path: split-K partial sums exceed the 2 GiB buffer range");
+    const float *rrms = nullptr;
+    if (v.rms) {
+        const int rc = launch_row_rms(gu, X, ws, l, v, st, &rrms);
+        if (rc)
+            return rc;
+    }
+    void *H = ws + l.h_off;
+    GemmFusedParams fp;
+    fp.gate_up = gemm_params(gu, Wg, Wu, X, H, ws, l, v, rrms, nullptr);
+    fp.down = gemm_params(dn, Wd, nullptr, H, Y, ws, l, Variant{}, nullptr, nullptr);
+    fp.down.counters = fp.gate_up.counters + gu.tile_count;
+    fp.down.partial = reinterpret_cast<float *>(ws + l.partial_off + align_up(gu.partial_bytes));
+    fp.ready = reinterpret_cast<uint32_t *>(ws + l.counters_off + kStripCounterBytes);
+    fp.errors = reinterpret_cast<uint32_t *>(ws + l.counters_off + kErrorOffset);
+    fp.spin_limit = g_spin_limit.load();
+    const dim3 grid(fused_grid(plan));
+    static_assert(FusedDownTiny::BMW == DownTiny::BMW && FusedDownTiny::BN == DownTiny::BN &&
+                      FusedDownTiny::BK == DownTiny::BK && FusedDownMid::BMW == DownMid::BMW &&
+                      FusedDownMid::BN == DownMid::BN && FusedDownMid::BK == DownMid::BK,
+                  "the fused down steps run the planned tiles");
+    if (tiny)
+        hipLaunchKernelGGL((gemm_fused_kernel<GateUpTiny, FusedDownTiny>), grid, dim3(GateUpTiny::NTHREADS), 0, st,
+                           fp);
+    else
+        hipLaunchKernelGGL((gemm_fused_kernel<GateUpMid, FusedDownMid>), grid, dim3(GateUpMid::NTHREADS), 0, st, fp);
+    return hip_check(hipGetLastError(), "fused MFMA kernel launch");
 }
 
 template <bool RMS>
@@ -308,9 +371,9 @@ int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t b
         snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", name, blocks, threads, splits);
         text += tmp;
     };
-    if (plan.path == GMLP_PATH_FUSED) {
-        const std::string name = "gemv_fused_kernel<" + std::to_string(T) + ", false>";
-        line(name.c_str(), fused_grid(plan), kGemvThreads, plan.gate_up.splits);
+    if (plan.path == GMLP_PATH_FUSED || plan.path == GMLP_PATH_FUSED_MFMA) {
+        const std::string name = fused_kernel_name(plan);
+        line(name.c_str(), fused_grid(plan), plan.gate_up.threads, plan.gate_up.splits);
         snprintf(buf, bytes, "%s", text.c_str());
         return ok();
     }
@@ -382,6 +445,10 @@ int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const vo
     if (plan.path == GMLP_PATH_FUSED) {
         rc = v.rms ? launch_fused<true>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st)
                    : launch_fused<false>(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
+        return rc ? rc : ok();
+    }
+    if (plan.path == GMLP_PATH_FUSED_MFMA) {
+        rc = launch_fused_mfma(plan, X, Wg, Wu, Wd, Y, ws, l, v, st);
         return rc ? rc : ok();
     }
     void *H = ws + l.h_off;

@@ -56,12 +56,20 @@ using GateUpTiny = GemmShape<2, 4, 1, 1, 1, 4, 64>; // 128 F cols x 32 tokens, 4
 using DownTiny = GemmShape<1, 4, 1, 1, 1, 6, 64>;   // 128 D cols x 32 tokens, 4 waves
 using GateUpMid = GemmShape<2, 4, 1, 1, 2, 3, 64>;  // 128 F cols x 64 tokens, 4 waves
 using DownMid = GemmShape<1, 4, 1, 1, 2, 6, 64>;    // 128 D cols x 64 tokens, 4 waves
+// The down steps of the one-launch MFMA kernel: the same tiles with 4 LDS
+// stages, so that one LDS array per stage, shared with the gate/up step's,
+// fits a CU (the ring depth does not change any sum: same bits).
+using FusedDownTiny = GemmShape<1, 4, 1, 1, 1, 4, 64>;
+using FusedDownMid = GemmShape<1, 4, 1, 1, 2, 4, 64>;
 // Column tiles swept per token tile by consecutive blocks (L2 locality),
 // from a sweep at T=4096/2048 on MI355X.
 constexpr int kGroupGateUp = 8;
 constexpr int kGroupDown = 8;
 
 constexpr int kGemvMaxTokens = 8;
+// The one-launch MFMA path (GMLP_PATH_FUSED_MFMA) runs the 32- and 64-token
+// tiles: one token tile per step.
+constexpr int kFusedMfmaMaxTokens = 64;
 // The automatic path takes the GEMV kernels up to this many tokens.  From 7
 // tokens the 32-token MFMA tiles are faster (measured at D = 4096,
 // F = 14336: 70.7 us against 74.6 us at T = 7 and 76.7 us at T = 8; equal at
@@ -285,6 +293,16 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         gemv_step(p.down, (int)D, (int)T, (int)F, 1);
         return p;
     }
+    if (path == GMLP_PATH_FUSED_MFMA) { // the few-token tiles whatever F and D are
+        if (T <= GateUpTiny::BN) {
+            gemm_step<GateUpTiny>(p.gate_up, K_GEMM_GU_T, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
+            gemm_step<DownTiny>(p.down, K_GEMM_DN_T, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+        } else {
+            gemm_step<GateUpMid>(p.gate_up, K_GEMM_GU_M, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
+            gemm_step<DownMid>(p.down, K_GEMM_DN_M, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+        }
+        return p;
+    }
     // Gate/up: large tiles once there are enough of them to fill the chip,
     // and above 256 tokens once they at least nearly fill it: there one
     // round of large tiles beats the partial second round that small tiles
@@ -310,6 +328,13 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     return p;
 }
 
+// Whether both steps' split-K counters of a one-launch MFMA plan fit in the
+// counter block together (down's follow gate/up's).
+bool fused_mfma_counters_fit(const Plan &p)
+{
+    return (size_t)(p.gate_up.tile_count + p.down.counters) * sizeof(uint32_t) <= kStripCounterBytes;
+}
+
 // One layout serves every path, so a workspace sized by gmlp_workspace_size
 // fits whichever kernels run.
 Layout make_layout(int64_t T, int64_t D, int64_t F)
@@ -327,6 +352,16 @@ Layout make_layout(int64_t T, int64_t D, int64_t F)
         partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes});
         if (path == GMLP_PATH_GEMV) // the fused kernel runs both steps at once: separate partial sums
             partial = std::max(partial, align_up(p.gate_up.partial_bytes) + p.down.partial_bytes);
+    }
+    if (T <= kFusedMfmaMaxTokens) {
+        // The one-launch MFMA path: both steps' partial sums and counters at
+        // once (where its counters fit the block: otherwise the path refuses
+        // the shape and the other paths keep their workspace).
+        const Plan p = make_plan(T, D, F, GMLP_PATH_FUSED_MFMA);
+        if (fused_mfma_counters_fit(p)) {
+            counters = std::max(counters, p.gate_up.tile_count + p.down.counters);
+            partial = std::max(partial, align_up(p.gate_up.partial_bytes) + p.down.partial_bytes);
+        }
     }
     Layout l;
     l.counters_off = 0;
@@ -415,11 +450,15 @@ int check_variant(int activation, float beta, int rmsnorm, float eps, Variant *v
 
 int check_path(int path, int64_t T)
 {
-    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA && path != GMLP_PATH_FUSED)
+    if (path != GMLP_PATH_AUTO && path != GMLP_PATH_GEMV && path != GMLP_PATH_MFMA && path != GMLP_PATH_FUSED &&
+        path != GMLP_PATH_FUSED_MFMA)
         return fail(GMLP_ERR_INVALID_ARG, "unknown path %d", path);
     if ((path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) && T > kGemvMaxTokens)
         return fail(GMLP_ERR_UNSUPPORTED, "%s path needs T <= %d (T=%lld)",
                     path == GMLP_PATH_GEMV ? "GEMV" : "fused", kGemvMaxTokens, (long long)T);
+    if (path == GMLP_PATH_FUSED_MFMA && T > kFusedMfmaMaxTokens)
+        return fail(GMLP_ERR_UNSUPPORTED, "fused MFMA path needs T <= %d (T=%lld)", kFusedMfmaMaxTokens,
+                    (long long)T);
     return GMLP_OK;
 }
 
@@ -427,8 +466,8 @@ int check_path(int path, int64_t T)
 // fused form.
 int check_single_step_path(int path, int64_t T)
 {
-    if (path == GMLP_PATH_FUSED)
-        return fail(GMLP_ERR_UNSUPPORTED, "the fused path runs the whole Gated MLP only");
+    if (path == GMLP_PATH_FUSED || path == GMLP_PATH_FUSED_MFMA)
+        return fail(GMLP_ERR_UNSUPPORTED, "the fused paths run the whole Gated MLP only");
     return check_path(path, T);
 }
 
@@ -474,6 +513,16 @@ std::string kernel_name(const Step &s, bool gate_up)
         return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
     default: return "none";
     }
+}
+
+// The kernel of a fused plan as a profiler names it, without the namespace.
+std::string fused_kernel_name(const Plan &plan)
+{
+    if (plan.path == GMLP_PATH_FUSED)
+        return "gemv_fused_kernel<" + std::to_string(plan.gate_up.N) + ", false>";
+    if (plan.gate_up.kind == K_GEMM_GU_T)
+        return "gemm_fused_kernel<" + shape_name<GateUpTiny>() + ", " + shape_name<FusedDownTiny>() + ">";
+    return "gemm_fused_kernel<" + shape_name<GateUpMid>() + ", " + shape_name<FusedDownMid>() + ">";
 }
 
 // The describe lines of a step: its launch, then its tail launch if any.

@@ -32,8 +32,9 @@ LIBRARY = os.path.join(HERE, "libgmlp.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "gmlp.h")
 HEADERS = [HEADER, os.path.join(os.path.dirname(HERE), "include", "softmax_matmul.h")]
 
-PATH_AUTO, PATH_GEMV, PATH_MFMA, PATH_FUSED = 0, 1, 2, 3
-_PATHS = {"auto": PATH_AUTO, "gemv": PATH_GEMV, "mfma": PATH_MFMA, "fused": PATH_FUSED}
+PATH_AUTO, PATH_GEMV, PATH_MFMA, PATH_FUSED, PATH_FUSED_MFMA = 0, 1, 2, 3, 4
+_PATHS = {"auto": PATH_AUTO, "gemv": PATH_GEMV, "mfma": PATH_MFMA, "fused": PATH_FUSED,
+          "fused_mfma": PATH_FUSED_MFMA}
 ACT_SILU, ACT_SWISH, ACT_SIGMOID = 0, 1, 2
 ACTIVATIONS = {"silu": ACT_SILU, "swish": ACT_SWISH, "sigmoid": ACT_SIGMOID}
 

@@ -71,14 +71,30 @@ int main()
                            l.h_off >= kCounterBytes,
                        "layout of T=%lld D=%lld F=%lld", (long long)T, (long long)D, (long long)F);
                 EXPECT(l.partial_off - l.h_off >= (size_t)T * F * 2, "H fits");
-                for (int path : {GMLP_PATH_AUTO, GMLP_PATH_GEMV, GMLP_PATH_MFMA, GMLP_PATH_FUSED}) {
+                for (int path : {GMLP_PATH_AUTO, GMLP_PATH_GEMV, GMLP_PATH_MFMA, GMLP_PATH_FUSED,
+                                 GMLP_PATH_FUSED_MFMA}) {
                     if (check_path(path, T) != GMLP_OK)
                         continue;
                     const Plan p = make_plan(T, D, F, path);
                     check_step(p.gate_up, l, T, D, F);
                     check_step(p.down, l, T, D, F);
-                    if (p.path == GMLP_PATH_FUSED)
+                    if (p.path == GMLP_PATH_FUSED || p.path == GMLP_PATH_FUSED_MFMA)
                         EXPECT(fused_grid(p) == p.gate_up.blocks + p.down.blocks, "fused grid");
+                    if (p.path == GMLP_PATH_FUSED_MFMA) {
+                        // Both steps' counters and partial sums are live at once.
+                        EXPECT(p.gate_up.tiles_n == 1 && p.down.tiles_n == 1, "one token tile");
+                        // Where the counters fit (else the launch refuses the
+                        // path), the layout holds both steps at once.
+                        if (fused_mfma_counters_fit(p)) {
+                            EXPECT(p.gate_up.tile_count + p.down.counters <= l.counters, "fused counters");
+                            EXPECT(align_up(p.gate_up.partial_bytes) + p.down.partial_bytes <=
+                                       l.rrms_off - l.partial_off,
+                                   "fused partial sums");
+                        }
+                        EXPECT((size_t)l.counters * 4 <= kStripCounterBytes, "layout counters fit");
+                        EXPECT(p.down.splits <= kFusedMaxSplits, "fused splits");
+                        EXPECT(!fused_kernel_name(p).empty(), "fused name");
+                    }
                     ++plans;
                 }
                 // Softmax+MatMul with M = T, K = F, N = D.

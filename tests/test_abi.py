@@ -130,7 +130,8 @@ def test_describe_rejects_bad_arguments(lib):
     buf = ctypes.create_string_buffer(64)
     assert lib.gmlp_describe(4, 260, 512, 0, buf, 64) == 2
     assert lib.gmlp_describe(9, 256, 512, 1, buf, 64) == 2  # GEMV needs T <= 8
-    assert lib.gmlp_describe(4, 256, 512, 4, buf, 64) == 1  # unknown path
+    assert lib.gmlp_describe(4, 256, 512, 5, buf, 64) == 1  # unknown path
+    assert lib.gmlp_describe(65, 256, 512, 4, buf, 64) == 2  # fused MFMA needs T <= 64
     assert lib.gmlp_describe(4, 256, 512, 0, None, 64) == 1
     assert lib.gmlp_describe(4, 256, 512, 0, buf, 8) == 0 and len(buf.value) == 7  # truncated
 
