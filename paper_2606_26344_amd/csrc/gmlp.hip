@@ -195,6 +195,8 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
     const Variant plain;
     switch (s.kind) {
     case K_GEMM_DN_L: {
+        if (s.splits > 1)
+            return launch_gemm<DownLarge, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
         const int rc = launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
                                                                  st);
         if (rc || !s.tail_tiles)

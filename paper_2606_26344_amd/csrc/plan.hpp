@@ -167,6 +167,8 @@ struct Variant {
 constexpr int kBlockTarget = 256;
 // Splits of a tail launch (see Step::tail_tiles).
 constexpr int kMaxTailSplits = 8;
+// Rows of K each split of a split-K large down tile keeps at least.
+constexpr int kMinLargeSplitRows = 40 * DownLarge::BK;
 
 // Split K so that at most `target` blocks run (the small-T kernels hold one
 // block per CU: a second round of blocks would cost a whole tile's time),
@@ -317,8 +319,21 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         gemm_step<GateUpMid>(p.gate_up, K_GEMM_GU_M, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
     else
         gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
-    if (cdiv(T, DownLarge::BN) * cdiv(D, DownLarge::BMW) >= 192)
+    // Down: large tiles once there are enough of them to fill the chip.
+    // Above one token tile, from 40 of them up to a round, large tiles split over K to fill one
+    // round beat two rounds of 128 x 128 tiles (measured: D = 4096, F = 14336
+    // at T = 640 and 2048 6-8% faster, T = 1024 equal; D = 8192, F = 28672 at
+    // T = 512..1280 6-15% faster), while each split keeps at least 40
+    // k-tiles (D = 2048, F = 8192 at T = 2048, 4 splits of 32 k-tiles: 10%
+    // slower).
+    const int64_t down_large = cdiv(T, DownLarge::BN) * cdiv(D, DownLarge::BMW);
+    Step large_down;
+    if (T > DownLarge::BN && down_large >= 40 && down_large < 192)
+        gemm_step<DownLarge>(large_down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+    if (down_large >= 192)
         gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false, kGroupDown);
+    else if (large_down.kind == K_GEMM_DN_L && (large_down.splits == 1 || large_down.k_split >= kMinLargeSplitRows))
+        p.down = large_down;
     else if (T <= DownTiny::BN)
         gemm_step<DownTiny>(p.down, K_GEMM_DN_T, (int)D, (int)T, (int)F, 1, true, kGroupDown);
     else if (T <= DownMid::BN)
@@ -500,7 +515,8 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_GU_L: return "gemm_mfma_kernel<" + shape_name<GateUpLarge>() + ", 0, false, false>";
     case K_GEMM_GU_S:
         return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
-    case K_GEMM_DN_L: return "gemm_mfma_kernel<" + shape_name<DownLarge>() + ", 1, false, false>";
+    case K_GEMM_DN_L:
+        return "gemm_mfma_kernel<" + shape_name<DownLarge>() + (s.splits > 1 ? ", 1, true, false>" : ", 1, false, false>");
     case K_GEMM_DN_S:
         return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_T: return "gemm_mfma_kernel<" + shape_name<GateUpTiny>() + ", 0, true, true>";

@@ -317,3 +317,20 @@ def test_h_is_rounded_once_to_nearest_even(orc, T, D, F):
           % (T, D, F, 100 * same, int(steps.max())), flush=True)
     assert same >= 0.99
     assert steps.max() <= 1
+
+
+@pytest.mark.parametrize("T,D,F,splits", [(1280, 2056, 13000, 5), (2304, 4104, 264, 1)])
+def test_large_down_tiles_below_a_round(orc, T, D, F, splits):
+    # 40 to 191 tiles of 256 x 256 for the down step: split over K to fill a
+    # round (5 splits of 41 k-tiles for 45 tiles), or, with 129 tiles or
+    # more, one partial round without split-K.
+    (name, grid, block, k_splits) = gmlp.describe(T, D, F)[-1]
+    assert name.startswith("gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 4, 2, 64>") and k_splits == splits
+    _run(T, D, F, seed=T + D, rows=I.sample_rows(T, 48), orc=orc)
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=T + D)
+    args = [_dev(a) for a in (X, Wg, Wu, Wd)]
+    ws = gmlp.Workspace(T, D, F)
+    a = gmlp.forward(*args, workspace=ws).clone()
+    b = gmlp.forward(*args, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
