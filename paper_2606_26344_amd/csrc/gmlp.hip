@@ -180,6 +180,8 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     case K_GEMM_GU_M:
         return stream_weights(s) ? launch_gemm<GateUpMid, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
                                  : launch_gemm<GateUpMid, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+    case K_GEMM_GU_W: // one token tile: always streamed
+        return launch_gemm<GateUpMid96, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);
@@ -216,6 +218,8 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
                                                                                nullptr, rowdiv, st)
                                  : launch_gemm<DownMid, EPI_STORE, true, false>(s, Wd, nullptr, H, Y, ws, l, plain,
                                                                                 nullptr, rowdiv, st);
+    case K_GEMM_DN_W: // one token tile: always streamed
+        return launch_gemm<DownMid96, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);
     default: return fail(GMLP_ERR_INVALID_ARG, "no down kernel for this plan");
     }

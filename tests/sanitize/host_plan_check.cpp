@@ -56,7 +56,7 @@ static void check_step(const Step &s, const Layout &l, int64_t T, int64_t D, int
 int main()
 {
     const std::vector<int64_t> Ts = {1, 2, 3, 5, 6, 7, 8, 9, 15, 16, 17, 31, 32, 33, 48, 63, 64, 65,
-                                     100, 127, 128, 129, 200, 255, 256, 257, 300, 384, 511, 512, 640,
+                                     80, 96, 97, 100, 127, 128, 129, 200, 255, 256, 257, 300, 384, 511, 512, 640,
                                      768, 1000, 1024, 1280, 1536, 2048, 4096, 4352, 37601, 1 << 20, 1 << 24};
     const std::vector<int64_t> dims = {8, 72, 136, 256, 264, 520, 1032, 2056, 4096, 4104, 4352, 8192,
                                        14336, 14464, 28672, 1 << 16, 1 << 22};

@@ -116,8 +116,8 @@ def test_describe_names_the_kernels_of_each_path(lib):
     # One token tile (T = 128): split-K, and weights read once, so streamed.
     mid = gmlp.describe(128, 4096, 14336)
     assert mid[0][0].endswith(", 0, true, true>") and mid[1][0].endswith(", 1, true, true>")
-    # Up to 32 and up to 64 tokens: one tile of 32 or 64 tokens (streamed).
-    for T, bn in [(9, 32), (32, 32), (33, 64), (64, 64), (65, 128)]:
+    # Up to 32, 64 and 96 tokens: one tile of 32, 64 or 96 tokens (streamed).
+    for T, bn in [(9, 32), (32, 32), (33, 64), (64, 64), (65, 96), (96, 96), (97, 128)]:
         for name, *_ in gmlp.describe(T, 4096, 14336):
             wm, wn, tm, tn = [int(v) for v in name.split("<")[2].split(",")[1:5]]
             assert wn * tn * 32 == bn and name.endswith(", true, true>"), (T, name)

@@ -68,8 +68,9 @@ RAGGED = [
     (7, 256, 1032), (8, 264, 264), (9, 256, 512), (15, 264, 520), (16, 520, 1032),
     (17, 520, 1032), (33, 72, 136), (127, 256, 520), (128, 264, 1032), (129, 520, 264),
     (255, 256, 264), (257, 264, 520), (300, 1032, 2056),
-    # 32- and 64-token tiles (T <= 32, T <= 64), at their edges.
-    (32, 264, 1032), (48, 4104, 2056), (64, 520, 264), (65, 264, 520),
+    # 32-, 64- and 96-token tiles (T <= 32, T <= 64, T <= 96), at their edges.
+    (32, 264, 1032), (48, 4104, 2056), (64, 520, 264), (65, 264, 520), (80, 1032, 264),
+    (96, 264, 1032), (97, 520, 264),
 ]
 
 
@@ -90,10 +91,10 @@ def test_hidden_activations_past_2_gib(orc):
 
 
 def _random_shapes(n, seed):
-    # Token counts over every plan (GEMV, 32/64/128-token tiles, two token
+    # Token counts over every plan (GEMV, 32/64/96/128-token tiles, two token
     # tiles, 256-token tiles), D and F multiples of 8 up to 2056.
     r = np.random.default_rng(seed)
-    t_choices = [1, 2, 3, 4, 5, 6, 7, 8, 9, 31, 32, 33, 64, 65, 127, 128, 129, 200, 256, 257, 384, 600]
+    t_choices = [1, 2, 3, 4, 5, 6, 7, 8, 9, 31, 32, 33, 64, 65, 96, 97, 127, 128, 129, 200, 256, 257, 384, 600]
     return [(int(r.choice(t_choices)), 8 * int(r.integers(1, 258)), 8 * int(r.integers(1, 258)))
             for _ in range(n)]
 
@@ -257,10 +258,10 @@ def test_full_size_workload(orc, name, nrows):
     _run(w.T, w.D, w.F, seed=w.seed, rows=rows, unit_rms=w.unit_rms_rows, orc=orc)
 
 
-@pytest.mark.parametrize("T", [16, 48])
+@pytest.mark.parametrize("T", [16, 48, 80])
 def test_few_token_tiles_at_model_dims(orc, T):
-    # The 32- and 64-token tile configurations at the decode model's D and F
-    # (split-K over D = 4096 and F = 14336), on sampled rows.
+    # The 32-, 64- and 96-token tile configurations at the decode model's D
+    # and F (split-K over D = 4096 and F = 14336), on sampled rows.
     _run(T, 4096, 14336, seed=60 + T, rows=I.sample_rows(T, 8), orc=orc)
 
 
