@@ -18,8 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libgmlp.so")
 SOURCES = [os.path.join(CSRC, "gmlp.hip")]
-HEADERS = [os.path.join(CSRC, f) for f in ("common.hpp", "gemm_mfma.hpp", "gemv.hpp", "rmsnorm.hpp",
-                                                     "softmax.hpp", "tiling.hpp", "plan.hpp")] + [
+HEADERS = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith(".hpp")] + [
     os.path.join(INCLUDE, h) for h in ("gmlp.h", "softmax_matmul.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
