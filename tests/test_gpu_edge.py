@@ -16,7 +16,7 @@ from paper_2606_26344_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
 
-PATHS = [(3, "gemv"), (2, "fused"), (5, "mfma"), (64, "auto"), (300, "auto")]
+PATHS = [(3, "gemv"), (2, "fused"), (5, "mfma"), (64, "auto"), (80, "auto"), (128, "auto"), (300, "auto")]
 
 
 @pytest.fixture(scope="module", autouse=True)
