@@ -59,7 +59,7 @@ enum gmlp_status {
 
 /* Which kernels compute the call (gmlp_forward_ex). */
 enum gmlp_path {
-    GMLP_PATH_AUTO = 0,  /* GEMV for T <= 6, MFMA GEMMs otherwise (measured faster from T = 7) */
+    GMLP_PATH_AUTO = 0,  /* GEMV for T <= 5, MFMA GEMMs otherwise (measured faster from T = 6) */
     GMLP_PATH_GEMV = 1,  /* split-K streaming GEMV kernels; needs T <= 8 */
     GMLP_PATH_MFMA = 2,  /* MFMA GEMM kernels (any T) */
     GMLP_PATH_FUSED = 3, /* the whole MLP in one GEMV kernel: the first blocks run the gate/up

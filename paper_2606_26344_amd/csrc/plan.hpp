@@ -76,11 +76,13 @@ constexpr int kGemvMaxTokens = 8;
 // The one-launch MFMA path (GMLP_PATH_FUSED_MFMA) runs the 32- and 64-token
 // tiles: one token tile per step.
 constexpr int kFusedMfmaMaxTokens = 64;
-// The automatic path takes the GEMV kernels up to this many tokens.  From 7
+// The automatic path takes the GEMV kernels up to this many tokens.  From 6
 // tokens the 32-token MFMA tiles are faster (measured at D = 4096,
-// F = 14336: 70.7 us against 74.6 us at T = 7 and 76.7 us at T = 8; equal at
-// T = 6), since a GEMV load batch shrinks to two rows there.
-constexpr int kGemvAutoTokens = 6;
+// F = 14336 over rotated weights: 70.0-70.4 us against 72.5-73.7 us at
+// T = 6, 70.2 against 75.4-76.4 at T = 7; the GEMV wins at T = 5, 64.7
+// against 69.9), since a GEMV load batch shrinks to four rows from T = 3
+// and to two from T = 7.
+constexpr int kGemvAutoTokens = 5;
 constexpr int64_t kMaxDim = int64_t(1) << 22; // D, F: keeps 32-bit tile offsets in range
 // Tokens per call, and elements of any one tensor (2^37 bf16 = 256 GiB, more
 // than one device holds).  Together they keep every tile count, block count
