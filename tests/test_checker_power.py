@@ -12,12 +12,16 @@ same sampled rows the GPU tests check:
   * the activation dropped, g u;
   * one k-tile (32 rows of D) missing from the gate/up sums;
   * one k-tile (64 rows of F) missing from the down sum;
-  * G and U rounded to bf16 before the activation (an extra rounding step).
+  * G and U rounded to bf16 before the activation (an extra rounding step);
+  * H converted to fp16 but stored where the down step reads bf16 (the
+    wrong conversion instruction in the epilogue).
 
 The GPU's numerics are emulated with numpy: float32 products and sums, H
 rounded once to bf16 (round to nearest even), Y rounded to bf16.  That
-emulation must pass; so must H kept in fp16 (three more mantissa bits than
-the prescribed bf16: more accurate, not a mistake).  H truncated to bf16
+emulation must pass; so must H kept in fp16 end to end, stored and read as
+fp16 (three more mantissa bits than the prescribed bf16: more accurate, not
+a mistake, so no tolerance could reject it; fp16 bits read as bf16 are a
+mistake and are rejected).  H truncated to bf16
 instead of rounded to nearest also stays within the rule (its error is at
 most one bf16 step, like rounding's); the GPU test
 test_h_is_rounded_once_to_nearest_even pins the rounding mode instead.
@@ -110,7 +114,13 @@ MISTAKES = {
     "one gate/up k-tile dropped": lambda e: _down(e, silu(e["G_drop"]) * e["U_drop"]),
     "one down k-tile dropped": lambda e: _drop_down_tile(e),
     "G and U rounded to bf16 before the activation": lambda e: _down(e, silu(bf16(e["G"])) * bf16(e["U"])),
+    "H stored as fp16 bits, read as bf16": lambda e: _fp16_bits_read_as_bf16(e),
 }
+
+
+def _fp16_bits_read_as_bf16(e):
+    bits = (silu(e["G"]) * e["U"]).astype(np.float16).view(np.uint16)
+    return bf16(I.bf16_bits_to_f32(bits) @ e["wd"])
 
 
 def _drop_down_tile(e):
