@@ -50,6 +50,10 @@ using GateUpLarge = GemmShape<2, 4, 2, 1, 4, 3, 32>; // 128 F cols x 256 tokens,
 using GateUpSmall = GemmShape<2, 4, 2, 1, 2, 3, 64>; // 128 F cols x 128 tokens, 8 waves
 using DownLarge = GemmShape<1, 4, 2, 2, 4, 2, 64>;   // 256 D cols x 256 tokens, 8 waves
 using DownSmall = GemmShape<1, 2, 2, 2, 2, 4, 64>;   // 128 D cols x 128 tokens
+// Above 256 tokens where few down tiles fill the chip only with short
+// splits: 256 x 128 tiles split over K (half the fp32 partial tile of
+// DownLarge for the last block of each tile to read back).
+using DownWide = GemmShape<1, 4, 2, 2, 2, 3, 64>;    // 256 D cols x 128 tokens, 8 waves
 // Up to 32 tokens: the same weight tiles with one 32-token tile, so the
 // activations staged per weight byte drop fourfold.
 using GateUpTiny = GemmShape<2, 4, 1, 1, 1, 4, 64>; // 128 F cols x 32 tokens, 4 waves
@@ -118,7 +122,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 enum Kind {
     K_NONE,
     K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T,
-    K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T,
+    K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMM_DN_X,
     K_GEMV
 };
 
@@ -182,6 +186,9 @@ constexpr int kBlockTarget = 256;
 constexpr int kMaxTailSplits = 8;
 // Rows of K each split of a split-K large down tile keeps at least.
 constexpr int kMinLargeSplitRows = 40 * DownLarge::BK;
+// Large down tiles split into pieces shorter than this give way to the
+// 256 x 128 tiles (64 k-tiles of 64 rows).
+constexpr int kWideDownBelowRows = 64 * DownLarge::BK;
 
 // Split K so that at most `target` blocks run (the small-T kernels hold one
 // block per CU: a second round of blocks would cost a whole tile's time),
@@ -345,9 +352,25 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     Step large_down;
     if (T > DownLarge::BN && down_large >= 40 && down_large < 192)
         gemm_step<DownLarge>(large_down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+    // Where the large tiles' splits would be shorter than 64 k-tiles, and
+    // above 256 tokens where they are not used at all, 256 x 128 tiles split
+    // over K in splits of at least 40 k-tiles (measured at D = 4096,
+    // F = 14336: down step 6-24% faster at T = 257..1024, the step 2-10%;
+    // D = 8192, F = 28672, whose large-tile splits are 7168 rows and more,
+    // keep the large tiles; T = 300, D = 1032, F = 2056 would split 11 ways
+    // into 187-row pieces: 45% slower, so excluded by the minimum).
+    Step wide;
+    if (T > 256 && down_large < 192)
+        gemm_step<DownWide>(wide, K_GEMM_DN_X, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+    const bool large_ok =
+        large_down.kind == K_GEMM_DN_L && (large_down.splits == 1 || large_down.k_split >= kMinLargeSplitRows);
+    const bool wide_ok = wide.kind == K_GEMM_DN_X && wide.splits >= 2 && wide.k_split >= kMinLargeSplitRows &&
+                         (!large_ok || large_down.k_split < kWideDownBelowRows);
     if (down_large >= 192)
         gemm_step<DownLarge>(p.down, K_GEMM_DN_L, (int)D, (int)T, (int)F, 1, false, kGroupDown);
-    else if (large_down.kind == K_GEMM_DN_L && (large_down.splits == 1 || large_down.k_split >= kMinLargeSplitRows))
+    else if (wide_ok)
+        p.down = wide;
+    else if (large_ok)
         p.down = large_down;
     else if (T <= DownTiny::BN)
         gemm_step<DownTiny>(p.down, K_GEMM_DN_T, (int)D, (int)T, (int)F, 1, true, kGroupDown);
@@ -534,6 +557,7 @@ std::string kernel_name(const Step &s, bool gate_up)
         return "gemm_mfma_kernel<" + shape_name<GateUpSmall>() + ", 0, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_DN_L:
         return "gemm_mfma_kernel<" + shape_name<DownLarge>() + (s.splits > 1 ? ", 1, true, false>" : ", 1, false, false>");
+    case K_GEMM_DN_X: return "gemm_mfma_kernel<" + shape_name<DownWide>() + ", 1, true, false>";
     case K_GEMM_DN_S:
         return "gemm_mfma_kernel<" + shape_name<DownSmall>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_T: return "gemm_mfma_kernel<" + shape_name<GateUpTiny>() + ", 0, true, true>";

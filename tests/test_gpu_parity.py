@@ -283,6 +283,22 @@ def test_tail_tiles_split_over_k(orc, T, D, F):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+@pytest.mark.parametrize("T,D,F", [(384, 4104, 14336), (600, 2056, 14344), (1280, 2056, 13000)])
+def test_wide_down_tiles_split_over_k(orc, T, D, F):
+    # Above 256 tokens, where few down tiles fill the chip only with short
+    # splits, 256 x 128 down tiles split over K (ragged T, D and F in the
+    # second shape); fixed-order reduction: a second call gives the same bits.
+    plan = gmlp.describe(T, D, F)
+    assert plan[-1][0] == "gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 2, 3, 64>, 1, true, false>" and plan[-1][3] > 1
+    _run(T, D, F, seed=T + D, rows=I.sample_rows(T, 24), orc=orc)
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=T + D)
+    args = [_dev(a) for a in (X, Wg, Wu, Wd)]
+    a = gmlp.forward(*args).clone()
+    b = gmlp.forward(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
 @pytest.mark.parametrize("T,D,F", [(257, 264, 12296), (300, 136, 24584), (513, 264, 12296)])
 def test_large_gate_up_tiles_above_256_tokens(orc, T, D, F):
     # Above 256 tokens the 256-token gate/up tiles are used once they nearly
@@ -320,11 +336,12 @@ def test_h_is_rounded_once_to_nearest_even(orc, T, D, F):
     assert steps.max() <= 1
 
 
-@pytest.mark.parametrize("T,D,F,splits", [(1280, 2056, 13000, 5), (2304, 4104, 264, 1)])
+@pytest.mark.parametrize("T,D,F,splits", [(1280, 4104, 13000, 3), (2304, 4104, 264, 1)])
 def test_large_down_tiles_below_a_round(orc, T, D, F, splits):
     # 40 to 191 tiles of 256 x 256 for the down step: split over K to fill a
-    # round (5 splits of 41 k-tiles for 45 tiles), or, with 129 tiles or
-    # more, one partial round without split-K.
+    # round (3 splits of 68 k-tiles for 85 tiles, where 256 x 128 tiles
+    # would take more than a round), or, with 129 tiles or more, one partial
+    # round without split-K.
     (name, grid, block, k_splits) = gmlp.describe(T, D, F)[-1]
     assert name.startswith("gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 4, 2, 64>") and k_splits == splits
     _run(T, D, F, seed=T + D, rows=I.sample_rows(T, 48), orc=orc)
