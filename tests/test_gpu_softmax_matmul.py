@@ -115,6 +115,14 @@ def test_matmul_tail_tiles_split_over_k(sorc):
     _run(sorc, M, K, N, seed=41, rows=I.sample_rows(M, 32))
 
 
+def test_matmul_on_wide_tiles_split_over_k(sorc):
+    # 3 x 17 = 51 tiles of 256 x 128, 5 splits of 52 k-tiles: the divide by
+    # the softmax sums in the split-K epilogue of the wide tiles.
+    M, K, N = 384, 16384, 4104
+    assert smm.describe(M, K, N)[-1][0] == "gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 2, 3, 64>, 1, true, false>"
+    _run(sorc, M, K, N, seed=43, rows=I.sample_rows(M, 24))
+
+
 def test_probabilities_past_2_gib(sorc):
     """X and P = exp(X - rowmax) of more than 2 GiB each (M = 131080,
     K = 8192): row and tile base addresses are formed in 64 bits.  The
