@@ -5,14 +5,16 @@
 // the rate at which the weights stream from HBM.  A work item streams a strip
 // of up to 256 weight columns over a slice of k rows:
 //
-//   * lane (l % 32) owns 8 adjacent columns (one 16-byte load per row); the
-//     two 32-lane halves of a wave and the 4 waves take rows k = g, g+8, ...
-//     (8 row groups), so a wave reads two 512-byte row segments per load
-//     instruction;
+//   * a lane owns 8 adjacent columns (one 16-byte load per row), and the
+//     block's row groups g = 0 .. RG-1 take rows in turn (GemvLayout): a row
+//     group is a wave reading one 1 KB row segment per load instruction
+//     (gate/up up to 4 tokens: 512-column strips) or a 32-lane half-wave
+//     reading 512 bytes (256-column strips);
 //   * the activations of a lane's rows are loaded into registers with its
 //     weights (no LDS staging, so no barrier stalls the first loads);
 //   * partial sums are reduced in a fixed order: across the two halves of
-//     the wave by a lane shuffle, across the 4 waves through LDS, and across
+//     a wave by a lane shuffle (half-wave row groups), across the waves
+//     through LDS in wave order, and across
 //     the split-K items of a strip by the last block to finish (arrival
 //     counter), which adds the per-item sums in split order;
 //   * each lane keeps two batches of 16-byte weight loads in flight (a
@@ -42,7 +44,7 @@ struct GemvParams {
     int k_split;     // rows per split (a multiple of the load batch span)
     int splits;
     int strips;
-    int strip_lanes; // lanes per row (8 columns each, <= 32): strip width 8 * strip_lanes
+    int strip_lanes; // lanes per row segment (8 columns each): strip width 8 * strip_lanes
     // Gate/up epilogue: activation (enum Activation) and swish slope.
     int activation;
     float beta;
@@ -68,8 +70,8 @@ constexpr int gemv_reduce_batch() { return NT * NW <= 4 ? 16 : 64 / (NT * NW); }
 // activations (RMSNorm), last-block flag.
 template <int NT, int NW>
 struct GemvShared {
-    float red[4][NW][NT][kGemvMaxStrip];
-    float ssq[4][NT];
+    float red[GemvLayout<NT, NW>::WAVES][NW][NT][GemvLayout<NT, NW>::STRIP];
+    float ssq[GemvLayout<NT, NW>::WAVES][NT];
     int last;
 };
 
@@ -97,7 +99,8 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                                           const Wait &wait = Wait{})
 {
     static_assert(!RMS || EPI == EPI_GATE_MUL, "RMSNorm belongs to the gate/up step");
-    constexpr int RG = 8; // row groups per block
+    using L = GemvLayout<NT, NW>;
+    constexpr int RG = L::RG; // row groups per block
     constexpr int U = gemv_batch_rows<NT>();
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int strip = item % p.strips;
@@ -108,11 +111,11 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     const int kb = split * p.k_split;
     const int nrows = min(K, kb + p.k_split) - kb;
 
-    const int col = (lane & 31) * 8;
-    const int rg = wave * 2 + (lane >> 5);
+    const int col = (tid % L::LANES) * 8;
+    const int rg = tid / L::LANES;
 
-    // Batch b covers rows [8*U*b, 8*U*(b+1)) of the split; row group rg takes
-    // the U consecutive rows from (8*b + rg)*U.  Every lane of the block runs
+    // Batch b covers rows [RG*U*b, RG*U*(b+1)) of the split; row group rg
+    // takes the U consecutive rows from (RG*b + rg)*U.  Every lane of the block runs
     // the same nb batches, the last of which may be partial.  A batch is one
     // load of the U activations of each token (issued first) and U weight
     // loads per weight, all unconditional, so the compiler counts them and
@@ -133,7 +136,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
         u32x4 w[U][NW];
     };
     auto load_x = [&](Batch &v, int b) __attribute__((always_inline)) {
-        const int r0 = (8 * b + rg) * U;
+        const int r0 = (RG * b + rg) * U;
         // Activation pieces of min(U, 8) rows lie wholly in or out of the
         // split (nrows is a multiple of 8, r0 of U).
 #pragma unroll
@@ -170,7 +173,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
         }
     };
     auto load_w = [&](Batch &v, int b) __attribute__((always_inline)) {
-        const int r0 = (8 * b + rg) * U;
+        const int r0 = (RG * b + rg) * U;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int r = min(r0 + u, nrows - 1);
@@ -220,7 +223,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
 
     {
         auto fma_batch = [&](const Batch &bt, int b) __attribute__((always_inline)) {
-            const int r0 = (8 * b + rg) * U;
+            const int r0 = (RG * b + rg) * U;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (r0 + u < nrows) {
@@ -264,24 +267,28 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
                 fma_batch(ring[i], b + i + DEPTH);
     }
 
-    // Row groups 2*wave and 2*wave+1 share columns: add the two wave halves.
+    // Half-wave row groups: groups 2*wave and 2*wave+1 share columns, so
+    // the two wave halves are added first.  (With 1 KB segments every lane
+    // of a wave reads the same rows.)
+    if constexpr (L::HALVES == 2) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w)
+        for (int w = 0; w < NW; ++w)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                acc[w][t][e] += __shfl_xor(acc[w][t][e], 32);
-    if constexpr (RMS) {
+                for (int e = 0; e < 8; ++e)
+                    acc[w][t][e] += __shfl_xor(acc[w][t][e], 32);
+        if constexpr (RMS)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-            ssq[t] += __shfl_xor(ssq[t], 32);
+            for (int t = 0; t < NT; ++t)
+                ssq[t] += __shfl_xor(ssq[t], 32);
+    }
+    if constexpr (RMS)
         if (lane == 0)
 #pragma unroll
             for (int t = 0; t < NT; ++t)
                 sh.ssq[wave][t] = ssq[t];
-    }
-    if (lane < 32) {
+    if (lane < L::LANES) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
@@ -294,16 +301,23 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     }
     __syncthreads();
 
-    // Thread tid now owns column m0 + tid of the strip.
+    // Thread tid < STRIP now owns column m0 + tid of the strip (threads past
+    // the strip, in blocks with more threads than columns, sum column 0 and
+    // store nothing); the waves' sums are added in wave order.
     const int m = m0 + tid;
     const bool mvalid = tid < width && m < M;
+    const int c = tid < L::STRIP ? tid : 0;
     float v[NW][NT];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-            v[w][t] = ((sh.red[0][w][t][tid] + sh.red[1][w][t][tid]) + sh.red[2][w][t][tid]) +
-                      sh.red[3][w][t][tid];
+        for (int t = 0; t < NT; ++t) {
+            float s = sh.red[0][w][t][c];
+#pragma unroll
+            for (int q = 1; q < L::WAVES; ++q)
+                s += sh.red[q][w][t][c];
+            v[w][t] = s;
+        }
     if (!ready)
 #pragma unroll
         for (int w = 0; w < NW; ++w)
@@ -313,8 +327,13 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     float ss[NT]; // RMS: the block's (then the whole row's) sum of x^2 per token
     if constexpr (RMS)
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
-            ss[t] = ((sh.ssq[0][t] + sh.ssq[1][t]) + sh.ssq[2][t]) + sh.ssq[3][t];
+        for (int t = 0; t < NT; ++t) {
+            float s = sh.ssq[0][t];
+#pragma unroll
+            for (int q = 1; q < L::WAVES; ++q)
+                s += sh.ssq[q][t];
+            ss[t] = s;
+        }
 
     if (p.splits > 1) {
         // Per-item sums go out with device-coherent stores; once they have
@@ -432,9 +451,9 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     return true;
 }
 
-// At most 256 VGPRs per lane: two blocks per CU stay resident.
+// At most 256 VGPRs per lane: two 4-wave blocks per CU stay resident.
 template <int NT, int NW, int EPI, bool RMS = false>
-__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__((GemvLayout<NT, NW>::THREADS)) __attribute__((amdgpu_waves_per_eu(2)))
 void gemv_splitk_kernel(GemvParams p)
 {
     __shared__ GemvShared<NT, NW> sh;
@@ -521,9 +540,10 @@ struct FusedWait {
 // strips of H, and read H with device-coherent loads.  Items and reductions
 // are those of the two-kernel GEMV path, so Y is bit for bit that path's.
 template <int NT, bool RMS>
-__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__((GemvLayout<NT, 2>::THREADS)) __attribute__((amdgpu_waves_per_eu(2)))
 void gemv_fused_kernel(GemvFusedParams p)
 {
+    static_assert(GemvLayout<NT, 2>::THREADS == GemvLayout<NT, 1>::THREADS, "one block size for both steps");
     __shared__ union {
         GemvShared<NT, 2> gate_up;
         GemvShared<NT, 1> down;

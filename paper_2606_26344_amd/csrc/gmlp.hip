@@ -118,7 +118,11 @@ int launch_gemv_nt(const Step &s, const void *w0, const void *w1, const void *ac
                    uint8_t *ws, const Layout &l, const Variant &v, const float *rowdiv, hipStream_t stream)
 {
     const GemvParams p = gemv_params(s, w0, w1, act, out, ws, l, v, rowdiv);
-    hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI, RMS>), dim3(s.blocks), dim3(kGemvThreads), 0,
+    using L = GemvLayout<NT, NW>;
+    if (s.threads != L::THREADS || s.strip_lanes != L::LANES)
+        return fail(GMLP_ERR_INVALID_ARG, "internal: GEMV plan for %d threads and %d lanes, kernel of %d and %d",
+                    s.threads, s.strip_lanes, L::THREADS, L::LANES);
+    hipLaunchKernelGGL((gemv_splitk_kernel<NT, NW, EPI, RMS>), dim3(s.blocks), dim3(L::THREADS), 0,
                        stream, p);
     return hip_check(hipGetLastError(), "GEMV launch");
 }
@@ -246,7 +250,8 @@ int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void 
     fp.ready = reinterpret_cast<uint32_t *>(ws + l.counters_off + kStripCounterBytes);
     fp.errors = reinterpret_cast<uint32_t *>(ws + l.counters_off + kErrorOffset);
     fp.spin_limit = g_spin_limit.load();
-    hipLaunchKernelGGL((gemv_fused_kernel<NT, RMS>), dim3(fused_grid(plan)), dim3(kGemvThreads), 0, st, fp);
+    hipLaunchKernelGGL((gemv_fused_kernel<NT, RMS>), dim3(fused_grid(plan)), dim3(GemvLayout<NT, 2>::THREADS), 0,
+                       st, fp);
     return hip_check(hipGetLastError(), "fused kernel launch");
 }
 

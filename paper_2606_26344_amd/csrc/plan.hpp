@@ -250,32 +250,35 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
                                (size_t)s.tail_splits * s.tail_tiles * tile_bytes);
 }
 
-// Rows per load batch of the 8 row groups, per token count (splits are
-// whole batches).
-int gemv_batch_span(int nt)
+// Rows per load batch of all row groups of a block, per token count and
+// step (splits are whole batches).
+int gemv_batch_span(int nt, int nw)
 {
+    const int rg = gemv_threads(nt) / gemv_strip_lanes(nt, nw);
     switch (nt) {
-    case 1: return 8 * gemv_batch_rows<1>();
-    case 2: return 8 * gemv_batch_rows<2>();
-    case 3: return 8 * gemv_batch_rows<3>();
-    case 4: return 8 * gemv_batch_rows<4>();
-    case 5: return 8 * gemv_batch_rows<5>();
-    case 6: return 8 * gemv_batch_rows<6>();
-    case 7: return 8 * gemv_batch_rows<7>();
-    default: return 8 * gemv_batch_rows<8>();
+    case 1: return rg * gemv_batch_rows<1>();
+    case 2: return rg * gemv_batch_rows<2>();
+    case 3: return rg * gemv_batch_rows<3>();
+    case 4: return rg * gemv_batch_rows<4>();
+    case 5: return rg * gemv_batch_rows<5>();
+    case 6: return rg * gemv_batch_rows<6>();
+    case 7: return rg * gemv_batch_rows<7>();
+    default: return rg * gemv_batch_rows<8>();
     }
 }
 
-// GEMV decomposition: strips of 256 columns (32 lanes x 8) times k splits.
-// Measured on MI355X at D=4096, F=14336 (T=1): one block per CU at most, as
-// few splits as that allows, and splits of whole load batches are fastest
-// (gate/up 56 strips x 4 splits, down 16 x 14: 224 blocks of 1024 rows);
-// more, shorter blocks add partial sums and reduction latency, and a second
-// block on a CU does not raise its share of HBM bandwidth.
+// GEMV decomposition: strips of 512 columns (64 lanes x 8: gate/up up to 4
+// tokens) or 256 columns (32 lanes x 8) times k splits.  Measured on MI355X
+// at D=4096, F=14336: one block per CU at most, as few splits as that
+// allows, and splits of whole load batches are fastest (T = 1: gate/up 28
+// strips x 8 splits of 512 rows, down 16 x 16 splits of 896 rows); more,
+// shorter blocks add partial sums and reduction latency (down in 28 or 32
+// splits: 2-4 us slower), and a second block on a CU does not raise its
+// share of HBM bandwidth.
 // For T = 7, 8 a load batch is only two rows (the accumulators of 8 tokens
-// take the registers), so two blocks per CU keep enough loads in flight
-// (measured: T = 5, 6 are 9% and 4% faster with one block per CU, T = 7, 8
-// 6% and 11% slower).
+// take the registers), so two 4-wave blocks per CU keep enough loads in
+// flight (measured: T = 5, 6 are 9% and 4% faster with one block per CU,
+// T = 7, 8 6% and 11% slower).
 int gemv_block_target(int nt) { return nt <= 6 ? 256 : 512; }
 
 void gemv_step(Step &s, int M, int N, int K, int nw)
@@ -284,10 +287,10 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
     s.M = M;
     s.N = N;
     s.K = K;
-    s.threads = kGemvThreads;
-    s.strip_lanes = 32;
+    s.threads = gemv_threads(N);
+    s.strip_lanes = gemv_strip_lanes(N, nw);
     s.strips = (int)cdiv(M, 8 * s.strip_lanes);
-    const int span = gemv_batch_span(N);
+    const int span = gemv_batch_span(N, nw);
     const int64_t max_sp = std::max<int64_t>(1, std::min<int64_t>(gemv_block_target(N) / s.strips, cdiv(K, span)));
     int64_t rows = 0;
     for (int64_t sp = max_sp; sp >= 1 && !rows; --sp)

@@ -47,14 +47,38 @@ struct GemmShape {
 };
 
 // ---- split-K GEMV (T <= 8) ---------------------------------------------------
-constexpr int kGemvMaxStrip = 256; // widest strip (32 lanes x 8 columns)
-constexpr int kGemvThreads = 256;
+// Block layouts.  Up to kGemvWideTokens tokens a block is 8 waves; the
+// gate/up step (two weights) gives each wave one 1 KB segment of a weight
+// row per load (64 lanes x 8 columns: 512-column strips, 8 row groups) and
+// the down step each 32-lane half of a wave a 512-byte segment (256-column
+// strips, 16 row groups).  Above, a block is 4 waves of 512-byte half-wave
+// segments (256-column strips, 8 row groups), which leaves the registers for
+// the accumulators of more tokens and lets two blocks share a CU.  Measured
+// on MI355X at D = 4096, F = 14336, same process: T = 1 step 59.3 against
+// 60.0 us (gate/up 37.4 against 38.2), T = 2 61.3 against 62.0, but T = 4
+// 64.1 against 62.8; for the down step 1 KB segments were slower (T = 1:
+// 21.8 against 21.3 us).
+constexpr int kGemvWideTokens = 2;
+template <int NT, int NW>
+struct GemvLayout {
+    static constexpr int THREADS = NT <= kGemvWideTokens ? 512 : 256;
+    static constexpr int LANES = NT <= kGemvWideTokens && NW == 2 ? 64 : 32; // lanes per row segment
+    static constexpr int STRIP = 8 * LANES;        // columns per strip, one per thread at most
+    static constexpr int WAVES = THREADS / 64;
+    static constexpr int RG = THREADS / LANES;     // row groups
+    static constexpr int HALVES = 64 / LANES;      // row groups per wave
+    static_assert(STRIP <= THREADS, "one column per thread in the reduction");
+};
+// Threads and lanes per row segment of the GEMV blocks (host side).
+constexpr int gemv_threads(int nt) { return nt <= kGemvWideTokens ? 512 : 256; }
+constexpr int gemv_strip_lanes(int nt, int nw) { return nt <= kGemvWideTokens && nw == 2 ? 64 : 32; }
 
 // Weight rows per lane per load batch (U), and batches in flight per lane
 // (DEPTH): DEPTH*NW*U loads of 16 bytes in flight per lane, within the
-// register budget of NT tokens.
+// register budget of NT tokens (with the 512-thread blocks, 128 KB in flight
+// per block at U = 4).
 template <int NT>
-constexpr int gemv_batch_rows() { return NT <= 2 ? 8 : NT <= 6 ? 4 : 2; }
+constexpr int gemv_batch_rows() { return NT <= 6 ? 4 : 2; }
 template <int NT>
 constexpr int gemv_depth() { return 2; }
 

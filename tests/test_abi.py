@@ -108,7 +108,7 @@ def test_describe_names_the_kernels_of_each_path(lib):
     assert [k[0] for k in gemv] == ["gemv_splitk_kernel<1, 2, 0, false>",
                                     "gemv_splitk_kernel<1, 1, 1, false>"]
     for name, grid, block, splits in gemv:
-        assert block == 256 and 128 < grid <= 256 and splits > 1
+        assert block == 512 and 128 < grid <= 256 and splits > 1  # 8-wave blocks up to 2 tokens
     big = gmlp.describe(4096, 4096, 14336)
     assert [k[0].split("<")[0] for k in big] == ["gemm_mfma_kernel", "gemm_mfma_kernel"]
     # <shape, epilogue, split-K, streamed weights>: prefill has neither.
@@ -139,9 +139,12 @@ def test_describe_rejects_bad_arguments(lib):
 @pytest.mark.parametrize("T", [1, 2, 3, 5, 8])
 @pytest.mark.parametrize("D,F", [(4096, 14336), (8192, 28672), (264, 520), (4104, 2056), (8, 8)])
 def test_gemv_plan_covers_k_with_at_most_one_round_of_blocks(lib, T, D, F):
-    for (name, grid, block, splits), (M, K) in zip(gmlp.describe(T, D, F, "gemv"), [(F, D), (D, F)]):
-        strips = -(-M // 256)
-        assert grid == strips * splits and block == 256
+    for step, ((name, grid, block, splits), (M, K)) in enumerate(zip(gmlp.describe(T, D, F, "gemv"),
+                                                                     [(F, D), (D, F)])):
+        # 8-wave blocks up to 2 tokens; gate/up strips of 512 columns there.
+        width = 512 if T <= 2 and step == 0 else 256
+        strips = -(-M // width)
+        assert grid == strips * splits and block == (512 if T <= 2 else 256)
         assert splits <= K // 8 + 1
         assert grid <= max(512, strips)
 
@@ -235,7 +238,7 @@ def test_fused_path_plan_and_validation(lib):
     gemv = gmlp.describe(1, 4096, 14336, "gemv")
     assert len(fused) == 1 and fused[0][0] == "gemv_fused_kernel<1, false>"
     # One block per item of either step: the gate/up items first.
-    assert fused[0][1] == sum(g[1] for g in gemv) and fused[0][2] == 256
+    assert fused[0][1] == sum(g[1] for g in gemv) and fused[0][2] == gemv[0][2] == 512
     assert fused[0][3] == gemv[0][3]
     for T in range(1, 9):
         (name, grid, block, splits), = gmlp.describe(T, 264, 520, "fused")

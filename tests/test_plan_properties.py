@@ -55,7 +55,7 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
     plan = gmlp.describe(T, D, F)
     steps = _steps(plan)
     assert [s for s, _ in steps] == [0, 1]
-    for (_, lines), (M, K) in zip(steps, [(F, D), (D, F)]):
+    for (step, lines), (M, K) in zip(steps, [(F, D), (D, F)]):
         for name, grid, block, splits in lines:
             assert grid >= 1 and splits >= 1 and block in (256, 512)
         name, grid, block, splits = lines[0]
@@ -63,7 +63,11 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
             # The automatic path takes the GEMV kernels up to 5 tokens.
             assert len(lines) == 1
             assert T <= 5 and name.startswith("gemv_splitk_kernel<%d," % T)
-            strips = _cdiv(M, 256)
+            # Up to 2 tokens: 8-wave blocks; the gate/up step reads 1 KB row
+            # segments (512-column strips), the down step 512 bytes (256).
+            # Above, 4-wave blocks of 256-column strips.
+            assert block == (512 if T <= 2 else 256)
+            strips = _cdiv(M, 512 if T <= 2 and step == 0 else 256)
             assert grid == strips * splits
             assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
             continue
