@@ -41,7 +41,12 @@ value in TFLOP/s of 2MKN, the matmul kernel as the dominant one.
 --path picks the kernel path (auto, gemv, mfma, or fused: the one-kernel
 decode path); --graph adds the step's time when captured in a HIP graph and
 replayed; --vendor-gemm adds the vendor library's time for the same matmul
-shapes (context).  Only one GPU is used: --gpus above 1 exits with a message.
+shapes (context).  The default run also times, after the workloads, a loop of
+MFMAs on register operands (paper_2606_26344_amd/mfma_ceiling, random and
+all-zero data): under the board's power limit the random-data rate is the
+ceiling of any GEMM on random data, reported beside the MFMA-bound records
+as roofline.power_capped_mfma (--mfma-ceiling prints it alone).  Only one
+GPU is used: --gpus above 1 exits with a message.
 """
 from __future__ import annotations
 
@@ -50,6 +55,7 @@ import ctypes
 import json
 import math
 import os
+import subprocess
 import sys
 import time
 
@@ -143,6 +149,9 @@ def parse_args(argv=None):
                         "shape), one JSON line per T and path; with --path auto also the GEMV, "
                         "MFMA and fused paths for T <= 8 and the MFMA and fused MFMA paths up "
                         "to T = 64")
+    p.add_argument("--mfma-ceiling", action="store_true",
+                   help="print the board's sustained bf16 MFMA rate on random and zero operands "
+                        "(the power-limited ceiling of the MFMA-bound steps) and exit")
     p.add_argument("--vendor-gemm", action="store_true",
                    help="also time torch.matmul (the vendor GEMM library) on the same two "
                         "matmul shapes, for context (X [T,D] x [Wg|Wu] [D,2F], H [T,F] x Wd)")
@@ -918,6 +927,32 @@ SUITE_KEYS = ("value", "unit", "ms_per_step", "steps", "warmup", "config", "roof
 SUITE_HEADLINE = "decode"
 
 
+MFMA_CEILING = os.path.join(HERE, "paper_2606_26344_amd", "mfma_ceiling")
+
+
+def mfma_ceiling(ms=20.0):
+    """The board's sustained bf16 matrix-core rate: mfma_ceiling (built with
+    the library) issues MFMAs back to back on register operands, random and
+    then all-zero, for about `ms` each.  Under the board's power limit the
+    random-data rate is what a GEMM on random data could reach at best; the
+    zero-data rate shows the clock-limited peak.  Context for the roofline,
+    not its peak (that stays the published dense peak)."""
+    import torch
+
+    if not os.path.exists(MFMA_CEILING):
+        return {"error": "mfma_ceiling is not built (python -m paper_2606_26344_amd.build)"}
+    if torch.cuda.is_initialized():
+        torch.cuda.synchronize()
+    res = subprocess.run([MFMA_CEILING, "%g" % ms], capture_output=True, text=True, timeout=120)
+    if res.returncode != 0:
+        return {"error": "mfma_ceiling exited with %d: %s" % (res.returncode, res.stderr.strip()[-200:])}
+    runs = [json.loads(ln) for ln in res.stdout.splitlines() if ln.startswith("{")]
+    out = {"ms_per_run": ms, "command": "paper_2606_26344_amd/mfma_ceiling %g" % ms}
+    for r in runs:
+        out["%s_data_tflops" % r["data"]] = r["tflops"]
+    return out
+
+
 def run_suite(args):
     """The default benchmark: one JSON line whose value is the decode
     workload's (T = 1, the configuration the HBM half of the metric is quoted
@@ -947,6 +982,16 @@ def run_suite(args):
         print("suite: %s %.3f %s, %.1f us per step" % (name, rec["value"], rec["unit"],
                                                        rec["ms_per_step"] * 1e3),
               file=sys.stderr, flush=True)
+    # The matrix-core ceiling under the board's power limit, next to the
+    # MFMA-bound records (measured once, after them).
+    ceiling = mfma_ceiling()
+    for rec in configs.values():
+        if rec["roofline"]["bound"] == "mfma":
+            ctx = dict(ceiling)
+            if "random_data_tflops" in ceiling:
+                ctx["frac_of_random_data_ceiling"] = round(
+                    rec["roofline"]["achieved"] / ceiling["random_data_tflops"], 4)
+            rec["roofline"]["power_capped_mfma"] = ctx
     result["config"]["suite"] = [SUITE_HEADLINE] + list(configs)
     result["configs"] = configs
     return result
@@ -956,6 +1001,9 @@ def main(argv=None):
     args = parse_args(argv)
     if args.summarize_profile:
         return summarize_profile(args)
+    if args.mfma_ceiling:
+        print(json.dumps(mfma_ceiling()), flush=True)
+        return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the Gated MLP here runs on a single MI355X "

@@ -18,6 +18,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libgmlp.so")
 SOURCES = [os.path.join(CSRC, "gmlp.hip")]
+# A measuring program beside the library (not part of it): the board's
+# sustained bf16 matrix-core rate, which bench.py reports as context.
+MFMA_CEILING = os.path.join(PKG, "mfma_ceiling")
+MFMA_CEILING_SOURCE = os.path.join(CSRC, "mfma_ceiling.hip")
 HEADERS = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC)) if f.endswith(".hpp")] + [
     os.path.join(INCLUDE, h) for h in ("gmlp.h", "softmax_matmul.h")]
 
@@ -37,10 +41,9 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra_flags=()) -> str:
-    """Compile libgmlp.so next to this file; returns its path."""
-    tmp = LIBRARY + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, *extra_flags, "-o", tmp, *SOURCES]
+def _compile(out, flags, sources, verbose):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, *flags, "-o", tmp, *sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -51,15 +54,24 @@ def build(verbose: bool = False, extra_flags=()) -> str:
         print("\n".join(shown), file=sys.stderr)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed with exit code %d" % res.returncode)
-    os.replace(tmp, LIBRARY)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False, extra_flags=()) -> str:
+    """Compile libgmlp.so (and the mfma_ceiling program) next to this file;
+    returns the library's path."""
+    _compile(LIBRARY, [*FLAGS, *extra_flags], SOURCES, verbose)
+    exe_flags = [f for f in FLAGS if f not in ("-shared", "-fPIC")]
+    _compile(MFMA_CEILING, exe_flags, [MFMA_CEILING_SOURCE], verbose)
     return LIBRARY
 
 
 def is_stale() -> bool:
-    if not os.path.exists(LIBRARY):
+    if not os.path.exists(LIBRARY) or not os.path.exists(MFMA_CEILING):
         return True
     t = os.path.getmtime(LIBRARY)
-    return any(os.path.getmtime(f) > t for f in SOURCES + HEADERS)
+    return (any(os.path.getmtime(f) > t for f in SOURCES + HEADERS) or
+            os.path.getmtime(MFMA_CEILING_SOURCE) > os.path.getmtime(MFMA_CEILING))
 
 
 if __name__ == "__main__":

@@ -23,3 +23,18 @@ def test_parse_rejects_missing_or_unreadable_fields():
     assert bench.parse_smi_csv("") is None
     assert bench.parse_smi_csv("gpu,gfx_0_clk\n0,1600\n") is None      # no socket_power
     assert bench.parse_smi_csv(HEADER + "\n" + _row("N/A", [1600] * 8)) is None
+
+
+def test_mfma_ceiling_reads_the_program_output(tmp_path, monkeypatch):
+    # A stand-in for the measuring program: the wrapper runs it with the run
+    # length and keeps the rate of each data kind (no GPU involved).
+    fake = tmp_path / "mfma_ceiling"
+    fake.write_text("#!/bin/sh\n"
+                    "echo '{\"data\": \"random\", \"ms\": 20.1, \"tflops\": 1702.5, \"frac_nominal\": 0.6765, \"iters\": 9}'\n"
+                    "echo '{\"data\": \"zero\", \"ms\": 14.0, \"tflops\": 2450.0, \"frac_nominal\": 0.9735, \"iters\": 9}'\n")
+    fake.chmod(0o755)
+    monkeypatch.setattr(bench, "MFMA_CEILING", str(fake))
+    got = bench.mfma_ceiling(20.0)
+    assert got["random_data_tflops"] == 1702.5 and got["zero_data_tflops"] == 2450.0
+    monkeypatch.setattr(bench, "MFMA_CEILING", str(tmp_path / "missing"))
+    assert "error" in bench.mfma_ceiling()
