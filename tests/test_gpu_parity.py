@@ -144,6 +144,20 @@ def test_small_T_on_the_mfma_path(orc, T):
     _run(T, 264, 520, seed=40 + T, path="mfma", orc=orc)
 
 
+# Up to 2 tokens the gate/up GEMV streams 512-column strips with one 1 KB row
+# segment per wave and the down GEMV 256-column strips in 16 half-wave row
+# groups: strips cut short by F or D, a single 8-column strip, splits shorter
+# than one load batch (32 or 64 rows) and a last split cut short by K.
+WIDE_GEMV = [(1, 8, 8), (1, 40, 1032), (2, 1032, 8), (2, 4104, 520), (1, 264, 14344), (2, 72, 24584)]
+
+
+@pytest.mark.parametrize("T,D,F", WIDE_GEMV, ids=["T%dD%dF%d" % s for s in WIDE_GEMV])
+def test_eight_wave_gemv_strips(orc, T, D, F):
+    plan = gmlp.describe(T, D, F)
+    assert plan[0][0].startswith("gemv") and plan[0][2] == 512 and plan[1][2] == 512
+    _run(T, D, F, seed=3 * T + D + F, orc=orc)
+
+
 @pytest.mark.parametrize("T", [1, 3, 8])
 def test_gemv_path_explicitly(orc, T):
     _run(T, 4104, 2056, seed=50 + T, path="gemv", orc=orc)
