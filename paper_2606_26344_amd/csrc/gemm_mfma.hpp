@@ -432,6 +432,51 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             return -1;
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (NW == 1 && PIECES > 16) {
+            // Large store tiles: the last block reads its own partial sums
+            // back as well, so the accumulators are dead once stored, and
+            // sums each pass of CH pieces over the splits (in order 0, 1,
+            // 2, ...: the same sums as below, its own pieces being the bits
+            // it stored) and stores that pass's outputs before the next.
+            // Keeping the accumulators live through the reduction and the
+            // epilogue spilled registers.
+            constexpr int CH = 8;
+            static_assert(PIECES % CH == 0, "whole passes");
+            const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.out + (size_t)n0 * M + m0);
+#pragma unroll
+            for (int c0 = 0; c0 < PIECES; c0 += CH) {
+                f32x4 sum[CH];
+                for (int sp = 0; sp < p.splits; ++sp) {
+                    const uint32_t base = wave_base(sp);
+                    f32x4 x[CH];
+#pragma unroll
+                    for (int g = 0; g < CH; ++g)
+                        x[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                             prs, lane_off, base + (c0 + g) * 1024u, kCoherent));
+#pragma unroll
+                    for (int g = 0; g < CH; ++g)
+                        sum[g] = sp == 0 ? x[g] : sum[g] + x[g];
+                }
+#pragma unroll
+                for (int g = 0; g < CH; ++g) {
+                    // Piece c0 + g holds accumulators 4j .. 4j+3 of acc[0][mi][ni].
+                    const int mi = (c0 + g) / (4 * TN) % TM, ni = (c0 + g) / 4 % TN, j = (c0 + g) % 4;
+                    const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                    const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[e] = sum[g][e];
+                        if (EPI == EPI_STORE && p.rowdiv)
+                            v[e] = v[e] / (n0 + tl < N ? p.rowdiv[n0 + tl] : 1.0f);
+                    }
+                    const uint32_t off = n0 + tl < N && m0 + fl < M ? (uint32_t)(tl * M + fl) * 2u : kOutOfRange;
+                    __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}, ro,
+                                                          off, 0, OUT_POLICY);
+                }
+            }
+            return m0;
+        }
         // Pieces are summed CH at a time: all of them for up to 16; the
         // 256 x 256 tiles take four passes of 8, which keeps the loaded
         // pieces and the sums within the register budget next to the
