@@ -389,7 +389,7 @@ def run_workload(name, args):
         result["copy_calibration_bytes"] = COPY_BYTES
         del src, dst
     if args.vendor_gemm:
-        result["vendor_gemm"] = vendor_gemm(T, D, F, args, wsets[0], x, stream)
+        result["vendor_gemm"] = vendor_gemm(T, D, F, args, wsets, x, stream)
     if args.power > 0:
         result["power"] = power_samples(step, args.power, stream)
     if not args.no_cpu_baseline:
@@ -738,38 +738,39 @@ def run_softmax_matmul(name, args):
     return result
 
 
-def vendor_gemm(T, D, F, args, weights, x, stream):
+def vendor_gemm(T, D, F, args, wsets, x, stream):
     """The vendor library's time for the two matmul shapes of a step (no
     activation, no fusion): context for the MFMA kernels, not a baseline of
     the method.  Both weights of the first matmul are concatenated into one
     [D, 2F] operand, so it is one library call as the fused kernel is one
-    launch."""
+    launch.  Consecutive calls rotate through the same weight copies as the
+    step, so that the 256 MB Infinity Cache serves neither."""
     import torch
 
-    wg, wu, wd = weights
-    w2 = torch.cat([wg, wu], dim=1).contiguous()
+    w2s = [torch.cat([wg, wu], dim=1).contiguous() for wg, wu, _ in wsets]
+    wds = [wd for _, _, wd in wsets]
     h = torch.empty((T, F), dtype=torch.bfloat16, device=x.device).normal_()
 
     def timed(fn, k):
-        for _ in range(args.warmup):
-            fn()
+        for i in range(args.warmup):
+            fn(i)
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        for _ in range(k):
-            fn()
+        for i in range(k):
+            fn(i)
         b.record(stream)
         torch.cuda.synchronize()
         return a.elapsed_time(b) / k
 
-    gu_ms = timed(lambda: torch.matmul(x, w2), args.steps)
-    dn_ms = timed(lambda: torch.matmul(h, wd), args.steps)
+    gu_ms = timed(lambda i: torch.matmul(x, w2s[i % len(w2s)]), args.steps)
+    dn_ms = timed(lambda i: torch.matmul(h, wds[i % len(wds)]), args.steps)
     out = {"library": "torch.matmul (" + ("hipBLASLt" if torch.version.hip else "vendor") + ")",
            "gate_up_us": round(gu_ms * 1e3, 3), "down_us": round(dn_ms * 1e3, 3),
            "gate_up_tflops": round(4.0 * T * D * F / (gu_ms / 1e3) / 1e12, 3),
            "down_tflops": round(2.0 * T * D * F / (dn_ms / 1e3) / 1e12, 3)}
-    del w2, h
+    del w2s, wds, h
     return out
 
 

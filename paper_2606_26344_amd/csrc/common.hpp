@@ -17,6 +17,7 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 enum Epilogue {
     EPI_GATE_MUL = 0, // out = bf16(act(acc0) * acc1)    (H of the gate/up step)
     EPI_STORE = 1,    // out = bf16(acc0)                (Y of the down step)
+    EPI_GATE_PAIR = 2, // out = bf16(act(G) * U), G and U from the two blocks of a pair
 };
 
 #define GMLP_LDS(p) ((__attribute__((address_space(3))) void *)(p))

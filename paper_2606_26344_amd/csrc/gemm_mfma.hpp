@@ -13,6 +13,12 @@
 //     paper's reorder of the RMSNorm multiply past the matmul, Section 2);
 //     G and U never leave registers.
 //   * down:            NW = 1 (Wd), epilogue writes Y = bf16(H Wd).
+//   * paired gate/up:  NW = 1; the two blocks of a pair stream one weight
+//     each (Wg or Wu) over the whole of K, for the same column tile, and the
+//     later of the two combines its accumulators with the other's into
+//     H = bf16(act(r G) * (r U)), through the split-K exchange below.  Each
+//     block reads 256-byte row segments of one weight, with no fp32 partial
+//     sums of K halves to exchange.
 //
 // Data flow per k-step of BK:
 //   global --(buffer_load ... lds, 16 B per lane, zero-filled out of range)-->
@@ -181,8 +187,12 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     const int tile = local;
     const int M = p.M, N = p.N, K = p.K;
     const int m0 = tm * S::BMW, n0 = tn * S::BN;
-    const int kb = split * p.k_split;
-    const int ke = min(K, kb + p.k_split);
+    // A pair's blocks each take the whole of K; split selects the weight.
+    constexpr bool PAIR = EPI == EPI_GATE_PAIR;
+    static_assert(!PAIR || (NW == 1 && SPLIT), "a pair is two blocks of one weight each");
+    const int kb = PAIR ? 0 : split * p.k_split;
+    const int ke = PAIR ? K : min(K, kb + p.k_split);
+    const uint16_t *w_first = PAIR && split ? p.w1 : p.w0;
     const int nk = (ke - kb + S::BK - 1) / S::BK;
     const bool ragged_k = (ke - kb) % S::BK != 0; // last k-tile is partial
 
@@ -224,7 +234,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
         const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.act + (size_t)n0 * K + k0);
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
-            const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? p.w0 : p.w1) + (size_t)k0 * M + m0);
+            const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? w_first : p.w1) + (size_t)k0 * M + m0);
 #pragma unroll
             for (int i = 0; i < S::W_LOADS; ++i) {
                 const uint32_t v = (masked && i * S::W_RPI + w_k >= krem) ? kOutOfRange : w_voff;
@@ -432,6 +442,48 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             return -1;
         if (tid == 0)
             __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (PAIR) {
+            // This block's accumulators are G (split 0) or U (split 1); the
+            // other block's are read back piece by piece, and every piece
+            // gives 4 columns of H at once.
+            static_assert(PIECES <= 16, "the other block's pieces are read in one pass");
+            const uint32_t obase = wave_base(1 - split);
+            f32x4 other[PIECES];
+#pragma unroll
+            for (int g = 0; g < PIECES; ++g)
+                other[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, lane_off,
+                                                                                          obase + g * 1024u,
+                                                                                          kCoherent));
+            float rs[TN];
+#pragma unroll
+            for (int ni = 0; ni < TN; ++ni) {
+                const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
+                rs[ni] = p.rrms && t < N ? p.rrms[t] : 1.0f;
+            }
+            const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.out + (size_t)n0 * M + m0);
+#pragma unroll
+            for (int g = 0; g < PIECES; ++g) {
+                const int mi = g / (4 * TN) % TM, ni = g / 4 % TN, j = g % 4;
+                const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
+                const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
+                const float r = rs[ni];
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float own = acc[0][mi][ni][4 * j + e];
+                    float gv = split == 0 ? own : other[g][e], uv = split == 0 ? other[g][e] : own;
+                    if (p.rrms) {
+                        gv *= r;
+                        uv *= r;
+                    }
+                    v[e] = gate_act(gv, p.activation, p.beta) * uv;
+                }
+                const uint32_t off = n0 + tl < N && m0 + fl < M ? (uint32_t)(tl * M + fl) * 2u : kOutOfRange;
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}, ro,
+                                                      off, 0, OUT_POLICY);
+            }
+            return m0;
+        }
         if constexpr (NW == 1 && PIECES > 16) {
             // Large store tiles: the last block reads its own partial sums
             // back as well, so the accumulators are dead once stored, and

@@ -186,6 +186,13 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
                                  : launch_gemm<GateUpMid, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_W: // one token tile: always streamed
         return launch_gemm<GateUpMid96, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+    case K_GEMM_GU_P: // one token tile, a G and a U block per column tile
+        if (s.splits != 2 || s.tiles_n != 1)
+            return fail(GMLP_ERR_INVALID_ARG, "internal: paired gate/up plan with %d splits, %d token tiles",
+                        s.splits, s.tiles_n);
+        if (s.N <= PairMid96::BN)
+            return launch_gemm<PairMid96, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        return launch_gemm<PairSmall, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);

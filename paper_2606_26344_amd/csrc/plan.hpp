@@ -71,6 +71,11 @@ using DownMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>;   // 128 D cols x 96 tokens, 
 // fits a CU (the ring depth does not change any sum: same bits).
 using FusedDownTiny = GemmShape<1, 4, 1, 1, 1, 4, 64>;
 using FusedDownMid = GemmShape<1, 4, 1, 1, 2, 4, 64>;
+// The paired gate/up tiles (one weight per block, a G and a U block per
+// column tile, EPI_GATE_PAIR) for one token tile of 65 to 128 tokens: the
+// down step's tiles (with 3 stages at 128 tokens: 0.3 us faster than 4).
+using PairMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>; // 128 F cols x 96 tokens, 4 waves
+using PairSmall = GemmShape<1, 2, 2, 2, 2, 3, 64>; // 128 F cols x 128 tokens, 4 waves
 // Column tiles swept per token tile by consecutive blocks (L2 locality),
 // from a sweep at T=4096/2048 on MI355X.
 constexpr int kGroupGateUp = 8;
@@ -121,7 +126,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 enum Kind {
     K_NONE,
-    K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T,
+    K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T, K_GEMM_GU_P,
     K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMM_DN_X,
     K_GEMV
 };
@@ -250,6 +255,44 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
                                (size_t)s.tail_splits * s.tail_tiles * tile_bytes);
 }
 
+// The paired gate/up step (EPI_GATE_PAIR): one-weight tiles, a G and a U
+// block per column tile, each over the whole of K.  It replaces a dual-B
+// plan that splits K in two where that plan's blocks fill more than three
+// quarters of the chip: the same blocks and weight bytes, half the fp32
+// exchange and 256-byte row segments of one weight per block, but each
+// block stages all of X rather than half.  Measured at D = 4096 over
+// rotated weights, gate/up alone (pairs against dual-B): 256 blocks
+// (F = 16384) T = 100 53.1 against 57.8 us, T = 128 54.4 against 62.0; 224
+// blocks (F = 14336) T = 65 48.9 against 51.3, T = 96 50.7-51.1 against
+// 52.5-52.9, T = 128 53.8-54.7 against 54.6-56.0; 192 blocks (F = 12288)
+// equal within 0.5%; 172 blocks (F = 11008) T = 100 47.1 against 45.1, where
+// fewer CUs share the stream and the extra staging costs.  Up to 64 tokens
+// (where the one-launch MFMA path runs the dual-B tiles) the gain is within
+// 1-2%, so those keep the dual-B plan.
+constexpr int kPairMinBlocks = kBlockTarget * 3 / 4 + 1;
+template <class S>
+void pair_step(Step &s, int M, int N, int K, int group_m)
+{
+    s.kind = K_GEMM_GU_P;
+    s.M = M;
+    s.N = N;
+    s.K = K;
+    s.tiles_m = (int)cdiv(M, S::BMW);
+    s.tiles_n = (int)cdiv(N, S::BN);
+    s.group_m = std::max(1, std::min(group_m, s.tiles_m));
+    const int tiles = s.tiles_m * s.tiles_n;
+    s.tile_count = tiles;
+    s.tail_tiles = 0;
+    s.tail_splits = 1;
+    s.tail_k_split = 0;
+    s.splits = 2; // the G and the U block of each tile
+    s.k_split = K;
+    s.blocks = 2 * tiles;
+    s.threads = S::NTHREADS;
+    s.counters = tiles;
+    s.partial_bytes = (size_t)2 * tiles * S::BMW * S::BN * sizeof(float);
+}
+
 // Rows per load batch of all row groups of a block, per token count and
 // step (splits are whole batches).
 int gemv_batch_span(int nt, int nw)
@@ -344,6 +387,13 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         gemm_step<GateUpMid96>(p.gate_up, K_GEMM_GU_W, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
     else
         gemm_step<GateUpSmall>(p.gate_up, K_GEMM_GU_S, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
+    if ((p.gate_up.kind == K_GEMM_GU_W || p.gate_up.kind == K_GEMM_GU_S) && p.gate_up.tiles_n == 1 &&
+        p.gate_up.splits == 2 && p.gate_up.blocks >= kPairMinBlocks) {
+        if (T <= PairMid96::BN)
+            pair_step<PairMid96>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
+        else
+            pair_step<PairSmall>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
+    }
     // Down: large tiles once there are enough of them to fill the chip.
     // Above one token tile, from 40 of them up to a round, large tiles split over K to fill one
     // round beat two rounds of 128 x 128 tiles (measured: D = 4096, F = 14336
@@ -571,6 +621,10 @@ std::string kernel_name(const Step &s, bool gate_up)
         return "gemm_mfma_kernel<" + shape_name<DownMid>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_W: return "gemm_mfma_kernel<" + shape_name<GateUpMid96>() + ", 0, true, true>";
     case K_GEMM_DN_W: return "gemm_mfma_kernel<" + shape_name<DownMid96>() + ", 1, true, true>";
+    case K_GEMM_GU_P: {
+        const std::string shape = s.N <= PairMid96::BN ? shape_name<PairMid96>() : shape_name<PairSmall>();
+        return "gemm_mfma_kernel<" + shape + ", 2, true, true>";
+    }
     case K_GEMV:
         return "gemv_splitk_kernel<" + std::to_string(s.N) + (gate_up ? ", 2, 0, false>" : ", 1, 1, false>");
     default: return "none";

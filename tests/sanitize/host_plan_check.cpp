@@ -31,8 +31,12 @@ static void check_step(const Step &s, const Layout &l, int64_t T, int64_t D, int
     EXPECT(s.kind != K_NONE, "T=%lld D=%lld F=%lld", (long long)T, (long long)D, (long long)F);
     EXPECT(s.blocks > 0 && s.threads > 0, "blocks %d threads %d", s.blocks, s.threads);
     EXPECT(s.splits >= 1 && s.k_split > 0, "splits %d k_split %d", s.splits, s.k_split);
-    EXPECT((int64_t)s.splits * s.k_split >= s.K && (int64_t)(s.splits - 1) * s.k_split < s.K,
-           "splits %d x %d vs K %d", s.splits, s.k_split, s.K);
+    if (s.kind == K_GEMM_GU_P) // both blocks of a pair take the whole of K
+        EXPECT(s.splits == 2 && s.k_split == s.K && s.tiles_n == 1, "pair of %d x %d vs K %d", s.splits,
+               s.k_split, s.K);
+    else
+        EXPECT((int64_t)s.splits * s.k_split >= s.K && (int64_t)(s.splits - 1) * s.k_split < s.K,
+               "splits %d x %d vs K %d", s.splits, s.k_split, s.K);
     EXPECT(s.partial_bytes <= l.rrms_off - l.partial_off, "partials %zu > %zu", s.partial_bytes,
            l.rrms_off - l.partial_off);
     EXPECT((size_t)s.counters * sizeof(uint32_t) <= kStripCounterBytes, "counters %d", s.counters);

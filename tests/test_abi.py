@@ -113,9 +113,13 @@ def test_describe_names_the_kernels_of_each_path(lib):
     assert [k[0].split("<")[0] for k in big] == ["gemm_mfma_kernel", "gemm_mfma_kernel"]
     # <shape, epilogue, split-K, streamed weights>: prefill has neither.
     assert big[0][0].endswith(", 0, false, false>") and big[1][0].endswith(", 1, false, false>")
-    # One token tile (T = 128): split-K, and weights read once, so streamed.
+    # One token tile (T = 128): split-K, and weights read once, so streamed;
+    # gate/up as pairs of one-weight blocks (epilogue 2) over the whole of K.
     mid = gmlp.describe(128, 4096, 14336)
-    assert mid[0][0].endswith(", 0, true, true>") and mid[1][0].endswith(", 1, true, true>")
+    assert mid[0][0].endswith(", 2, true, true>") and mid[1][0].endswith(", 1, true, true>")
+    assert mid[0][0].startswith("gemm_mfma_kernel<GemmShape<1,") and mid[0][1] == 224 and mid[0][3] == 2
+    # Up to 64 tokens the dual-B tiles split over K.
+    assert gmlp.describe(64, 4096, 14336)[0][0].endswith(", 0, true, true>")
     # Up to 32, 64 and 96 tokens: one tile of 32, 64 or 96 tokens (streamed).
     for T, bn in [(9, 32), (32, 32), (33, 64), (64, 64), (65, 96), (96, 96), (97, 128)]:
         for name, *_ in gmlp.describe(T, 4096, 14336):

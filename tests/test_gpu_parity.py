@@ -158,6 +158,30 @@ def test_eight_wave_gemv_strips(orc, T, D, F):
     _run(T, D, F, seed=3 * T + D + F, orc=orc)
 
 
+# 65 to 128 tokens where the dual-B gate/up tiles would split K in two over
+# more than 3/4 of the chip: a G and a U block per column tile, each over
+# the whole of K, the later of the two combining both into H.  96- and
+# 128-token tiles, K tails (D not a multiple of 64), last column tiles cut
+# short by F (F = 12424, 14344, 12296), the fewest (97) and most (128) pairs.
+PAIRED = [(65, 264, 12800), (96, 4104, 12424), (97, 264, 16384), (128, 1032, 14344), (112, 520, 12296)]
+
+
+@pytest.mark.parametrize("T,D,F", PAIRED, ids=["T%dD%dF%d" % s for s in PAIRED])
+def test_paired_gate_up_blocks(orc, T, D, F):
+    plan = gmlp.describe(T, D, F)
+    assert plan[0][0].endswith(", 2, true, true>") and plan[0][3] == 2, plan
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=T + D + F)
+    x, wg, wu, wd = (_dev(a) for a in (X, Wg, Wu, Wd))
+    ws = gmlp.Workspace(T, D, F)
+    rows = I.sample_rows(T, 24) if D * F > 2 ** 24 else np.arange(T)
+    h = gmlp.gate_up(x, wg, wu, workspace=ws)
+    y = gmlp.forward(x, wg, wu, wd, workspace=ws)
+    torch.cuda.synchronize()
+    Y_ref, H_ref = orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows, return_h=True)
+    _check(gmlp.to_bf16_bits(h)[rows], H_ref, "paired H T=%d D=%d F=%d" % (T, D, F))
+    _check(gmlp.to_bf16_bits(y)[rows], Y_ref, "paired Y T=%d D=%d F=%d" % (T, D, F))
+
+
 @pytest.mark.parametrize("T", [1, 3, 8])
 def test_gemv_path_explicitly(orc, T):
     _run(T, 4104, 2056, seed=50 + T, path="gemv", orc=orc)
@@ -212,7 +236,7 @@ def test_zero_tokens_leaves_output_untouched():
     assert torch.all(y == 3.0)
 
 
-@pytest.mark.parametrize("T,D,F", [(1, 4096, 14336), (64, 1032, 2056), (600, 512, 4104)])
+@pytest.mark.parametrize("T,D,F", [(1, 4096, 14336), (64, 1032, 2056), (100, 520, 12296), (600, 512, 4104)])
 def test_bitwise_deterministic(T, D, F):
     X, Wg, Wu, Wd = I.generate(T, D, F, seed=11)
     args = [_dev(a) for a in (X, Wg, Wu, Wd)]

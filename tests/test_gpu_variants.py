@@ -54,6 +54,14 @@ def test_variant_ragged_shapes(orc, name, T, D, F):
 
 
 @pytest.mark.parametrize("name", sorted(VARIANTS))
+def test_variant_paired_gate_up_blocks(orc, name):
+    # 100 tokens, 97 column tiles of F: the G and U blocks of a pair
+    # (activation and RMSNorm scale applied by the later one).
+    assert gmlp.describe(100, 520, 12296)[0][0].endswith(", 2, true, true>")
+    _run(orc, 100, 520, 12296, VARIANTS[name], seed=77, x_scale=3.0)
+
+
+@pytest.mark.parametrize("name", sorted(VARIANTS))
 @pytest.mark.parametrize("T", [2, 5])
 def test_variant_on_the_mfma_path_at_small_T(orc, name, T):
     _run(orc, T, 520, 1032, VARIANTS[name], seed=90 + T, path="mfma", x_scale=0.25)

@@ -41,7 +41,7 @@ def _steps(plan):
         if name.startswith("gemv"):
             step = 0 if name.split(",")[1].strip() == "2" else 1
         else:
-            step = _flags(name)[0]
+            step = {0: 0, 1: 1, 2: 0}[_flags(name)[0]]  # epilogue 2: the paired gate/up blocks
         if steps and steps[-1][0] == step:
             steps[-1][1].append(line)
         else:
@@ -85,6 +85,11 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
             if splits_i > 1:
                 assert split_k
                 assert splits_i * 4 * bmw * bn * 2 * (grid_i // splits_i) <= 2 ** 31  # partials addressable
+            if _flags(name_i)[0] == 2:
+                # A G and a U block per column tile of one token tile, where
+                # the dual-B plan would split K in two: 65 to 128 tokens.
+                assert step == 0 and splits_i == 2 and 65 <= T <= 128 and _cdiv(T, bn) == 1
+                assert 96 < grid_i // 2 <= 128  # two-way split of more than 3/4 of a round
         if len(lines) == 2:
             # Tail launch: whole rounds of 256 blocks first, then a partial
             # round of at most half the chip split over K.
