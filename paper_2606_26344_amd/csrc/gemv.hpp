@@ -40,6 +40,7 @@ struct GemvParams {
     uint16_t *out;       // [NT, M] bf16 (H, or Y)
     float *partial;      // [splits][NW][NT][M] fp32 per-item sums
     uint32_t *counters;  // arrival counter per strip (zero on entry and exit)
+    int counter_stride;  // words between two strips' counters
     int M, K;
     int k_split;     // rows per split (a multiple of the load batch span)
     int splits;
@@ -358,14 +359,14 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
         __syncthreads();
         if (tid == 0) {
             const uint32_t before =
-                __hip_atomic_fetch_add(p.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(p.counters + p.counter_stride * strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             sh.last = before == (uint32_t)(p.splits - 1);
         }
         __syncthreads();
         if (!sh.last)
             return false;
         if (tid == 0)
-            __hip_atomic_store(p.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(p.counters + p.counter_stride * strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (mvalid) {
             // Sum the splits in order 0, 1, 2, ...; the loads of C splits are
             // in flight at once (with RMSNorm, their sums of x^2 too, added

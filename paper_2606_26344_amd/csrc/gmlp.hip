@@ -103,6 +103,7 @@ GemvParams gemv_params(const Step &s, const void *w0, const void *w1, const void
     p.k_split = s.k_split;
     p.splits = s.splits;
     p.strips = s.strips;
+    p.counter_stride = s.counter_stride;
     p.strip_lanes = s.strip_lanes;
     p.activation = v.act;
     p.beta = v.beta;
@@ -246,13 +247,14 @@ int launch_fused_nt(const Plan &plan, const void *X, const void *Wg, const void 
     if (plan.down.splits > kFusedMaxSplits)
         return fail(GMLP_ERR_UNSUPPORTED, "fused path: %d down splits, at most %d", plan.down.splits,
                     kFusedMaxSplits);
-    if ((size_t)(plan.gate_up.strips + plan.down.strips) * sizeof(uint32_t) > kStripCounterBytes)
+    if ((size_t)(plan.gate_up.strips + plan.down.strips) * plan.gate_up.counter_stride * sizeof(uint32_t) >
+        kStripCounterBytes)
         return fail(GMLP_ERR_UNSUPPORTED, "fused path: too many strips for the counter block");
     void *H = ws + l.h_off;
     GemvFusedParams fp;
     fp.gate_up = gemv_params(plan.gate_up, Wg, Wu, X, H, ws, l, v, nullptr);
     fp.down = gemv_params(plan.down, Wd, nullptr, H, Y, ws, l, Variant{}, nullptr);
-    fp.down.counters = fp.gate_up.counters + plan.gate_up.strips;
+    fp.down.counters = fp.gate_up.counters + plan.gate_up.strips * plan.gate_up.counter_stride;
     fp.down.partial = reinterpret_cast<float *>(ws + l.partial_off + align_up(plan.gate_up.partial_bytes));
     fp.ready = reinterpret_cast<uint32_t *>(ws + l.counters_off + kStripCounterBytes);
     fp.errors = reinterpret_cast<uint32_t *>(ws + l.counters_off + kErrorOffset);

@@ -117,6 +117,7 @@ constexpr size_t kAlign = 256;
 // another shape.  Every kernel leaves the counters and ready words zero; the
 // give-up count stays until gmlp_workspace_status reads it.
 constexpr size_t kStripCounterBytes = 64 * 1024;
+constexpr int kCounterLine = 32; // words per 128-byte line
 constexpr size_t kReadyBytes = (size_t)kFusedMaxSplits * kFlagStride * sizeof(uint32_t);
 constexpr size_t kErrorOffset = kStripCounterBytes + kReadyBytes;
 constexpr size_t kCounterBytes = kErrorOffset + 256;
@@ -139,6 +140,7 @@ struct Step {
     int group_m = 1;              // GEMM block order
     int strips = 0;               // GEMV
     int strip_lanes = 32;         // GEMV: 8-column lanes per row
+    int counter_stride = 1;       // GEMV: words between two strips' arrival counters
     int splits = 1, k_split = 0;
     int blocks = 0, threads = 0;
     size_t partial_bytes = 0; // fp32 split-K partial sums
@@ -359,6 +361,20 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     if (path == GMLP_PATH_GEMV || path == GMLP_PATH_FUSED) {
         gemv_step(p.gate_up, (int)F, (int)T, (int)D, 2);
         gemv_step(p.down, (int)D, (int)T, (int)F, 1);
+        // Each strip's arrival counter on a 128-byte line of its own where
+        // both steps' counters fit so (the one-launch kernel holds them at
+        // once): the arrivals of one strip's splits then do not queue behind
+        // the other strips' atomics on a shared line.  Measured at the
+        // decode shape (16 down strips of 16 splits): down step 21.3 ->
+        // 20.3 us; the gate/up step (8 splits) unchanged.
+        const int stride = (size_t)(p.gate_up.strips + p.down.strips) * kCounterLine * sizeof(uint32_t) <=
+                                   kStripCounterBytes
+                               ? kCounterLine
+                               : 1;
+        for (Step *s : {&p.gate_up, &p.down}) {
+            s->counter_stride = stride;
+            s->counters = s->splits > 1 ? s->strips * stride : 0;
+        }
         return p;
     }
     if (path == GMLP_PATH_FUSED_MFMA) { // the few-token tiles whatever F and D are

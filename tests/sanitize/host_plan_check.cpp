@@ -42,6 +42,8 @@ static void check_step(const Step &s, const Layout &l, int64_t T, int64_t D, int
     EXPECT((size_t)s.counters * sizeof(uint32_t) <= kStripCounterBytes, "counters %d", s.counters);
     if (s.kind == K_GEMV) {
         EXPECT(s.strips * 8 * s.strip_lanes >= s.M, "strips %d", s.strips);
+        EXPECT(s.counter_stride == 1 || s.counter_stride == kCounterLine, "counter stride %d", s.counter_stride);
+        EXPECT(s.counters == (s.splits > 1 ? s.strips * s.counter_stride : 0), "GEMV counters %d", s.counters);
         EXPECT(s.blocks == s.strips * s.splits, "GEMV grid");
     } else {
         EXPECT((int64_t)s.tile_count + s.tail_tiles == (int64_t)s.tiles_m * s.tiles_n, "tiles %d + %d",

@@ -182,6 +182,16 @@ def test_paired_gate_up_blocks(orc, T, D, F):
     _check(gmlp.to_bf16_bits(y)[rows], Y_ref, "paired Y T=%d D=%d F=%d" % (T, D, F))
 
 
+# Each GEMV strip's arrival counter sits on a 128-byte line of its own
+# where both steps' counters fit the counter block so (up to 512 strips in
+# all); past that, on consecutive words.  514 strips (F = 262152): the
+# consecutive words, for both the two-kernel and the one-kernel path.
+@pytest.mark.parametrize("path", ["gemv", "fused"])
+def test_gemv_with_more_strips_than_counter_lines(orc, path):
+    T, D, F = 1, 264, 262152
+    _run(T, D, F, seed=61, path=path, orc=orc)
+
+
 @pytest.mark.parametrize("T", [1, 3, 8])
 def test_gemv_path_explicitly(orc, T):
     _run(T, 4104, 2056, seed=50 + T, path="gemv", orc=orc)
