@@ -934,10 +934,12 @@ MFMA_CEILING = os.path.join(HERE, "paper_2606_26344_amd", "mfma_ceiling")
 def mfma_ceiling(ms=20.0):
     """The board's sustained bf16 matrix-core rate: mfma_ceiling (built with
     the library) issues MFMAs back to back on register operands, random and
-    then all-zero, for about `ms` each.  Under the board's power limit the
-    random-data rate is what a GEMM on random data could reach at best; the
-    zero-data rate shows the clock-limited peak.  Context for the roofline,
-    not its peak (that stays the published dense peak)."""
+    then all-zero, for about `ms` each, with the GEMM kernels' instruction
+    (32x32x16: the plain keys) and with 16x16x32 (keys suffixed _16x16x32).
+    Under the board's power limit the random-data rate is what a GEMM on
+    random data could reach at best with that instruction; the zero-data rate
+    shows the clock-limited peak.  Context for the roofline, not its peak
+    (that stays the published dense peak)."""
     import torch
 
     if not os.path.exists(MFMA_CEILING):
@@ -950,7 +952,9 @@ def mfma_ceiling(ms=20.0):
     runs = [json.loads(ln) for ln in res.stdout.splitlines() if ln.startswith("{")]
     out = {"ms_per_run": ms, "command": "paper_2606_26344_amd/mfma_ceiling %g" % ms}
     for r in runs:
-        out["%s_data_tflops" % r["data"]] = r["tflops"]
+        # The GEMM kernels' instruction (32x32x16) under the plain keys.
+        suffix = "" if r.get("mfma", "32x32x16") == "32x32x16" else "_" + r["mfma"]
+        out["%s_data_tflops%s" % (r["data"], suffix)] = r["tflops"]
     return out
 
 

@@ -29,12 +29,13 @@ def test_mfma_ceiling_reads_the_program_output(tmp_path, monkeypatch):
     # A stand-in for the measuring program: the wrapper runs it with the run
     # length and keeps the rate of each data kind (no GPU involved).
     fake = tmp_path / "mfma_ceiling"
-    fake.write_text("#!/bin/sh\n"
-                    "echo '{\"data\": \"random\", \"ms\": 20.1, \"tflops\": 1702.5, \"frac_nominal\": 0.6765, \"iters\": 9}'\n"
-                    "echo '{\"data\": \"zero\", \"ms\": 14.0, \"tflops\": 2450.0, \"frac_nominal\": 0.9735, \"iters\": 9}'\n")
+    line = "echo '{\"mfma\": \"%s\", \"data\": \"%s\", \"ms\": 20.1, \"tflops\": %s, \"frac_nominal\": 0.7, \"iters\": 9}'\n"
+    fake.write_text("#!/bin/sh\n" + line % ("32x32x16", "random", "1702.5") + line % ("32x32x16", "zero", "2450.0")
+                    + line % ("16x16x32", "random", "2090.0") + line % ("16x16x32", "zero", "2470.0"))
     fake.chmod(0o755)
     monkeypatch.setattr(bench, "MFMA_CEILING", str(fake))
     got = bench.mfma_ceiling(20.0)
     assert got["random_data_tflops"] == 1702.5 and got["zero_data_tflops"] == 2450.0
+    assert got["random_data_tflops_16x16x32"] == 2090.0 and got["zero_data_tflops_16x16x32"] == 2470.0
     monkeypatch.setattr(bench, "MFMA_CEILING", str(tmp_path / "missing"))
     assert "error" in bench.mfma_ceiling()
