@@ -88,16 +88,57 @@ struct GemmParams {
 // Physical 16-byte chunk of logical chunk c in row k of a weight tile.  The
 // XOR keeps the 4 rows x 4 chunks read by 32 lanes of one transposing load
 // on distinct banks (and the 4 x 2 read by 16 lanes), for 64 or 32 banks.
-template <int CPR>
+template <int CPR, bool M16>
 __device__ __forceinline__ int w_swizzle(int k)
 {
-    if constexpr (CPR >= 16) {
+    if constexpr (CPR >= 16 && M16) {
+        // The 16x16x32 reads take rows k and k + 8 in one pass as well: the
+        // rows with bit 3 set use four other XOR values.
+        const int g = k & 3;
+        if (k & 8)
+            return g == 0 ? 2 : g == 1 ? 4 : g == 2 ? 8 : 14;
+        return g == 0 ? 0 : g == 1 ? 6 : g == 2 ? 10 : 12;
+    } else if constexpr (CPR >= 16) {
         const int g = k & 3;
         return g == 0 ? 0 : g == 1 ? 6 : g == 2 ? 10 : 12;
     } else {
         return (k & 3) << 1;
     }
 }
+
+// The accumulators of one 32 x 32 output block of a wave: one
+// v_mfma_f32_32x32x16_bf16 accumulator, or four v_mfma_f32_16x16x32_bf16
+// ones (subtile j: columns 16 (j & 1) .., tokens 16 (j >> 1) ..).  Piece j is
+// the lane's accumulators 4j .. 4j+3: 4 consecutive output columns of one
+// token, starting at column col(j) and token tok(j) of the block.
+template <bool M16>
+struct AccBlock;
+template <>
+struct AccBlock<false> {
+    f32x16 v;
+    __device__ float get(int r) const { return v[r]; }
+    __device__ void set(int r, float x) { v[r] = x; }
+    __device__ f32x4 piece(int j) const { return f32x4{v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]}; }
+    __device__ void set_piece(int j, const f32x4 &x)
+    {
+        v[4 * j] = x[0];
+        v[4 * j + 1] = x[1];
+        v[4 * j + 2] = x[2];
+        v[4 * j + 3] = x[3];
+    }
+    __device__ static int col(int j, int lane) { return 8 * j + 4 * (lane >> 5); }
+    __device__ static int tok(int, int lane) { return lane & 31; }
+};
+template <>
+struct AccBlock<true> {
+    f32x4 v[4];
+    __device__ float get(int r) const { return v[r >> 2][r & 3]; }
+    __device__ void set(int r, float x) { v[r >> 2][r & 3] = x; }
+    __device__ f32x4 piece(int j) const { return v[j]; }
+    __device__ void set_piece(int j, const f32x4 &x) { v[j] = x; }
+    __device__ static int col(int j, int lane) { return 16 * (j & 1) + 4 * (lane >> 4); }
+    __device__ static int tok(int j, int lane) { return 16 * (j >> 1) + (lane & 15); }
+};
 
 // Physical chunk of logical chunk c in LDS row r of an activation tile
 // (rows of 8 chunks): any 8, and any aligned 16, consecutive rows reading
@@ -198,13 +239,18 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
 
     // ---- staging addresses ---------------------------------------------------
     // Weight load i of this lane: row i*W_RPI + w_k, physical chunk lane %
-    // W_CPR holding logical chunk w_c.  The swizzle depends on the row only
-    // through row % 4, which is the same for every i, so one voffset serves
-    // all i and the row step goes into the scalar offset.
+    // W_CPR holding the logical chunk that the row's swizzle maps there.  The
+    // swizzle depends on the row only through bits 0, 1 and 3; bits 0 and 1
+    // are the same for every i, bit 3 too unless W_RPI = 8 (then it
+    // alternates), so one or two voffsets serve all i and the row step goes
+    // into the scalar offset.
     const int w_k = wave * S::W_LPR + lane / S::W_CPR;
-    const int w_c = (lane % S::W_CPR) ^ w_swizzle<S::W_CPR>(w_k);
-    const bool w_col_ok = m0 + w_c * 8 < M;
-    const uint32_t w_voff = w_col_ok ? (uint32_t)(w_k * M + w_c * 8) * 2u : kOutOfRange;
+    auto w_voff_of = [&](int row) __attribute__((always_inline)) {
+        const int c = (lane % S::W_CPR) ^ w_swizzle<S::W_CPR, S::M16>(row);
+        return m0 + c * 8 < M ? (uint32_t)(w_k * M + c * 8) * 2u : kOutOfRange;
+    };
+    const uint32_t w_voff = w_voff_of(w_k), w_voff_b3 = w_voff_of(w_k ^ 8);
+    static_assert(S::W_RPI % 16 == 0 || S::W_RPI == 8, "row bits 0, 1 fixed across loads, bit 3 fixed or alternating");
     const uint32_t w_soff_step = (uint32_t)S::W_RPI * (uint32_t)M * 2u;
     // Activation load i: LDS row x_r(i) (8 rows per wave load), physical
     // chunk lane % 8 holding chunk x_c of token x_t.  Tokens past N are
@@ -237,7 +283,9 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? w_first : p.w1) + (size_t)k0 * M + m0);
 #pragma unroll
             for (int i = 0; i < S::W_LOADS; ++i) {
-                const uint32_t v = (masked && i * S::W_RPI + w_k >= krem) ? kOutOfRange : w_voff;
+                const uint32_t v = (masked && i * S::W_RPI + w_k >= krem)      ? kOutOfRange
+                                   : (S::W_RPI == 8 && (i & 1)) ? w_voff_b3
+                                                                 : w_voff;
                 uint8_t *dst = sbuf + w * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024;
                 if constexpr (STREAM_W)
                     load16_to_lds_stream(rw, dst, v, (uint32_t)i * w_soff_step);
@@ -257,57 +305,78 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     };
 
     // ---- fragment read offsets ---------------------------------------------
-    // Weight (A) fragment of m-tile mi for k16 step kk: a transposing read of
-    // k rows kk*16 + r_lane (+4 for elements 4..7) in column chunk c.
-    const int r_lane = 8 * (lane >> 5) + ((lane & 15) >> 2);
-    int a_off[TM];
+    // 32x32x16: weight (A) fragment of m-tile mi for k16 step kk: a
+    // transposing read of k rows kk*16 + r_lane (+4 for elements 4..7) in
+    // column chunk c; each 16-lane group reads 4 rows x 16 columns, the two
+    // groups of a half-wave the two 16-column halves, the two half-waves k
+    // rows 0..7 and 8..15.  16x16x32: the 16-column half sa of m-tile mi for
+    // k32 step kk: the four 16-lane groups read k rows 8g .. 8g+7 of the
+    // same 16 columns.
+    constexpr bool M16 = S::M16;
+    constexpr int SUB = M16 ? 2 : 1; // 16-wide halves of a 32-wide block per fragment
+    using A = AccBlock<M16>;
+    const int r_lane = M16 ? 8 * (lane >> 4) + ((lane & 15) >> 2) : 8 * (lane >> 5) + ((lane & 15) >> 2);
+    int a_off[TM][SUB];
 #pragma unroll
-    for (int mi = 0; mi < TM; ++mi) {
-        const int c = wm * TM * 4 + mi * 4 + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
-        a_off[mi] = r_lane * S::W_ROW_BYTES + ((c ^ w_swizzle<S::W_CPR>(r_lane)) << 4) + (lane & 1) * 8;
-    }
-    // Token (B) fragment of n-tile ni: token t = wn*TN*32 + ni*32 + lane%32,
-    // logical chunk 2*kk + lane/32 of that token, i.e. LDS row t % X_ROWS,
-    // combined chunk 2*kk + lane/32 + X_CPT * (t / X_ROWS).  The chunk bits
-    // of the byte address are XORed with 32*kk for step kk.
-    int b_off[TN];
+    for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-        const int t = wn * TN * 32 + ni * 32 + (lane & 31);
-        const int r = t % S::X_ROWS;
-        const int cc = (lane >> 5) + S::X_CPT * (t / S::X_ROWS);
-        b_off[ni] = r * 128 + ((cc ^ x_swizzle(r)) << 4);
-    }
+        for (int sa = 0; sa < SUB; ++sa) {
+            const int c = wm * TM * 4 + mi * 4 + 2 * (M16 ? sa : (lane >> 4) & 1) + ((lane & 3) >> 1);
+            a_off[mi][sa] = r_lane * S::W_ROW_BYTES + ((c ^ w_swizzle<S::W_CPR, S::M16>(r_lane)) << 4) + (lane & 1) * 8;
+        }
+    // Token (B) fragment of n-tile ni (32x32x16): token t = wn*TN*32 + ni*32
+    // + lane%32, logical chunk 2*kk + lane/32 of that token, i.e. LDS row
+    // t % X_ROWS, combined chunk 2*kk + lane/32 + X_CPT * (t / X_ROWS); the
+    // chunk bits of the byte address are XORed with 32*kk for step kk.
+    // 16x16x32: half sb of n-tile ni, token t = wn*TN*32 + ni*32 + 16 sb +
+    // lane%16, chunk 4*kk + lane/16 (XOR 64*kk).
+    int b_off[TN][SUB];
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+        for (int sb = 0; sb < SUB; ++sb) {
+            const int t = wn * TN * 32 + ni * 32 + (M16 ? 16 * sb + (lane & 15) : lane & 31);
+            const int r = t % S::X_ROWS;
+            const int cc = (M16 ? lane >> 4 : lane >> 5) + S::X_CPT * (t / S::X_ROWS);
+            b_off[ni][sb] = r * 128 + ((cc ^ x_swizzle(r)) << 4);
+        }
 
-    f32x16 acc[NW][TM][TN];
+    A acc[NW][TM][TN];
 #pragma unroll
     for (int w = 0; w < NW; ++w)
 #pragma unroll
         for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
             for (int ni = 0; ni < TN; ++ni)
-                acc[w][mi][ni] = f32x16{};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[w][mi][ni].set_piece(j, f32x4{});
 
     struct Frags {
-        bf16x8 a[NW][TM];
-        bf16x8 b[TN];
+        bf16x8 a[NW][TM][SUB];
+        bf16x8 b[TN][SUB];
     };
     auto load_frags = [&](Frags &f, const uint8_t *sbuf, int kk) __attribute__((always_inline)) {
         const uint8_t *sx = sbuf + NW * S::W_TILE_BYTES;
 #pragma unroll
         for (int w = 0; w < NW; ++w)
 #pragma unroll
-            for (int mi = 0; mi < TM; ++mi) {
-                const uint8_t *pa = sbuf + w * S::W_TILE_BYTES + kk * 16 * S::W_ROW_BYTES + a_off[mi];
-                i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa));
-                i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa + 4 * S::W_ROW_BYTES));
-                f.a[w][mi] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            }
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int sa = 0; sa < SUB; ++sa) {
+                    const uint8_t *pa = sbuf + w * S::W_TILE_BYTES + kk * S::MFMA_K * S::W_ROW_BYTES + a_off[mi][sa];
+                    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa));
+                    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa + 4 * S::W_ROW_BYTES));
+                    f.a[w][mi][sa] =
+                        __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                }
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
-            f.b[ni] = *(const bf16x8 *)(sx + (b_off[ni] ^ (32 * kk)));
+#pragma unroll
+            for (int sb = 0; sb < SUB; ++sb)
+                f.b[ni][sb] = *(const bf16x8 *)(sx + (b_off[ni][sb] ^ (2 * S::MFMA_K * kk)));
     };
     auto mma = [&](const Frags &f) __attribute__((always_inline)) {
 #pragma unroll
@@ -315,9 +384,86 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
 #pragma unroll
             for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < TN; ++ni)
-                    acc[w][mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[w][mi], f.b[ni],
-                                                                             acc[w][mi][ni], 0, 0, 0);
+                for (int ni = 0; ni < TN; ++ni) {
+                    if constexpr (M16) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[w][mi][ni].v[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                f.a[w][mi][j & 1], f.b[ni][j >> 1], acc[w][mi][ni].v[j], 0, 0, 0);
+                    } else {
+                        acc[w][mi][ni].v = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[w][mi][0], f.b[ni][0],
+                                                                                   acc[w][mi][ni].v, 0, 0, 0);
+                    }
+                }
+    };
+    // 16x16x32: the A fragments of a k32 step are double-buffered (read for
+    // the next step among this step's MFMAs), the B fragments are not: each
+    // B fragment is read again for the next step right after the last of
+    // its 4 MFMAs (NW x TM x 2 of them), so the fragments take no more
+    // registers than the 32x32x16 ones.
+    struct FragA {
+        bf16x8 a[NW][TM][SUB];
+    };
+    struct FragB {
+        bf16x8 b[TN][SUB];
+    };
+    auto load_a = [&](FragA &f, const uint8_t *sbuf, int kk) __attribute__((always_inline)) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                for (int sa = 0; sa < SUB; ++sa) {
+                    const uint8_t *pa = sbuf + w * S::W_TILE_BYTES + kk * S::MFMA_K * S::W_ROW_BYTES + a_off[mi][sa];
+                    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa));
+                    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa + 4 * S::W_ROW_BYTES));
+                    f.a[w][mi][sa] =
+                        __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                }
+    };
+    auto load_b = [&](FragB &f, const uint8_t *sbuf, int kk, int ni, int sb) __attribute__((always_inline)) {
+        f.b[ni][sb] = *(const bf16x8 *)(sbuf + NW * S::W_TILE_BYTES + (b_off[ni][sb] ^ (2 * S::MFMA_K * kk)));
+    };
+    auto load_a1 = [&](FragA &f, const uint8_t *sbuf, int kk, int q) __attribute__((always_inline)) {
+        const int w = q / (TM * SUB), mi = q / SUB % TM, sa = q % SUB;
+        const uint8_t *pa = sbuf + w * S::W_TILE_BYTES + kk * S::MFMA_K * S::W_ROW_BYTES + a_off[mi][sa];
+        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa));
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4 *)GMLP_LDS(pa + 4 * S::W_ROW_BYTES));
+        f.a[w][mi][sa] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    // The MFMAs of one k32 step, one group per 16-token B fragment: its
+    // NW x TM x 2 MFMAs, then (A fragments spread over the groups) the next
+    // step's A reads and that B fragment's next read.  A scheduling fence
+    // after each group keeps every B read after the MFMAs that still need
+    // the old fragment, so the two never occupy registers at once.
+    auto mma_roll = [&](const FragA &fa, FragA &fa_next, FragB &fb, const uint8_t *nbuf, int nkk)
+                        __attribute__((always_inline)) {
+        constexpr int GROUPS = TN * SUB, AFRAGS = NW * TM * SUB;
+        constexpr int APG = (AFRAGS + GROUPS - 1) / GROUPS; // A fragments read per group
+        [&]<int... G>(std::integer_sequence<int, G...>) __attribute__((always_inline)) {
+            (
+                [&] {
+                    constexpr int ni = G / SUB, sb = G % SUB;
+                    if constexpr (M16)
+#pragma unroll
+                        for (int w = 0; w < NW; ++w)
+#pragma unroll
+                            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+                                for (int sa = 0; sa < SUB; ++sa)
+                                    acc[w][mi][ni].v[sa + 2 * sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                        fa.a[w][mi][sa], fb.b[ni][sb], acc[w][mi][ni].v[sa + 2 * sb], 0, 0, 0);
+#pragma unroll
+                    for (int q = G * APG; q < (G + 1) * APG && q < AFRAGS; ++q)
+                        load_a1(fa_next, nbuf, nkk, q);
+                    load_b(fb, nbuf, nkk, ni, sb);
+                    __builtin_amdgcn_sched_barrier(0);
+                }(),
+                ...);
+        }(std::make_integer_sequence<int, GROUPS>{});
     };
     // A tile has landed in LDS (for every wave) once at most the STAGES - 2
     // tiles issued after it are in flight and all waves have passed a
@@ -336,43 +482,63 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     // tile visible and frees this tile's buffer; the DMA of tile kt + STAGES
     // into it and the next tile's first fragment reads are then issued among
     // the last step's MFMAs.
-    static_assert(KSTEPS % 2 == 0, "k16 steps alternate between two fragment buffers");
+    static_assert(KSTEPS % 2 == 0, "k steps alternate between two fragment buffers");
+    static_assert(!M16 || KSTEPS == 2, "16x16x32: two k32 steps per k-tile");
     Frags f0, f1;
+    FragA fa0, fa1;
+    FragB fb;
     const bool ready = wait();
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
         (issue(stage_ptr(std::integral_constant<int, I>{}), I), ...);
     }(std::make_integer_sequence<int, STAGES - 1>{});
     wait_tile();
     issue(stage_ptr(std::integral_constant<int, STAGES - 1>{}), STAGES - 1);
-    load_frags(f0, stage_ptr(std::integral_constant<int, 0>{}), 0);
+    if constexpr (M16) {
+        load_a(fa0, stage_ptr(std::integral_constant<int, 0>{}), 0);
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+            for (int sb = 0; sb < SUB; ++sb)
+                load_b(fb, stage_ptr(std::integral_constant<int, 0>{}), 0, ni, sb);
+    } else {
+        load_frags(f0, stage_ptr(std::integral_constant<int, 0>{}), 0);
+    }
 
     // One k-tile held in stage buffer I, without branches: the registers
     // flow straight through (accumulators and fragments need no copies) and
-    // each k16 step is one scheduling region.  At the last tile the next-tile
+    // each k step is one scheduling region.  At the last tile the next-tile
     // fragment read touches stale LDS and is unused.
     auto step = [&](auto stage, int kt) __attribute__((always_inline)) {
         constexpr int I = decltype(stage)::value;
         uint8_t *buf = stage_ptr(stage);
-        [&]<int... KK>(std::integer_sequence<int, KK...>) __attribute__((always_inline)) {
-            (
-                [&] {
-                    // k16 step KK: fragments of step KK+1 among its MFMAs.
-                    if constexpr (KK % 2 == 0) {
-                        load_frags(f1, buf, KK + 1);
-                        mma(f0);
-                    } else {
-                        load_frags(f0, buf, KK + 1);
-                        mma(f1);
-                    }
-                    interleave_step<S::MFMAS, S::FRAG_READS, 0>();
-                }(),
-                ...);
-        }(std::make_integer_sequence<int, KSTEPS - 1>{});
-        wait_tile();
-        issue(buf, kt + STAGES);
-        load_frags(f0, stage_ptr(std::integral_constant<int, (I + 1) % STAGES>{}), 0);
-        mma(f1);
-        interleave_step<S::MFMAS, S::FRAG_READS, S::LOADS_PER_STAGE>();
+        uint8_t *next = stage_ptr(std::integral_constant<int, (I + 1) % STAGES>{});
+        if constexpr (M16) {
+            mma_roll(fa0, fa1, fb, buf, 1);
+            wait_tile();
+            issue(buf, kt + STAGES);
+            mma_roll(fa1, fa0, fb, next, 0);
+        } else {
+            [&]<int... KK>(std::integer_sequence<int, KK...>) __attribute__((always_inline)) {
+                (
+                    [&] {
+                        // k step KK: fragments of step KK+1 among its MFMAs.
+                        if constexpr (KK % 2 == 0) {
+                            load_frags(f1, buf, KK + 1);
+                            mma(f0);
+                        } else {
+                            load_frags(f0, buf, KK + 1);
+                            mma(f1);
+                        }
+                        interleave_step<S::MFMAS, S::FRAG_READS, 0>();
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, KSTEPS - 1>{});
+            wait_tile();
+            issue(buf, kt + STAGES);
+            load_frags(f0, next, 0);
+            mma(f1);
+            interleave_step<S::MFMAS, S::FRAG_READS, S::LOADS_PER_STAGE>();
+        }
     };
     int kt = 0;
     for (; kt + STAGES <= nk; kt += STAGES) {
@@ -395,7 +561,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
                 for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
-                        acc[w][mi][ni][e] = __builtin_nanf("");
+                        acc[w][mi][ni].set(e, __builtin_nanf(""));
 
     // ---- split-K: fixed-order reduction by the last block of each tile ----------
     // Each wave's partial sums go out as 16-byte device-coherent stores (sc1:
@@ -424,8 +590,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
                             const int g = ((w * TM + mi) * TN + ni) * 4 + j;
-                            const f32x4 v = {acc[w][mi][ni][4 * j], acc[w][mi][ni][4 * j + 1],
-                                             acc[w][mi][ni][4 * j + 2], acc[w][mi][ni][4 * j + 3]};
+                            const f32x4 v = acc[w][mi][ni].piece(j);
                             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, lane_off,
                                                                    base + g * 1024u, kCoherent);
                         }
@@ -454,23 +619,25 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
                 other[g] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, lane_off,
                                                                                           obase + g * 1024u,
                                                                                           kCoherent));
-            float rs[TN];
+            float rs[TN][SUB];
 #pragma unroll
-            for (int ni = 0; ni < TN; ++ni) {
-                const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-                rs[ni] = p.rrms && t < N ? p.rrms[t] : 1.0f;
-            }
+            for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+                for (int h = 0; h < SUB; ++h) {
+                    const int t = n0 + wn * TN * 32 + ni * 32 + A::tok(2 * h, lane);
+                    rs[ni][h] = p.rrms && t < N ? p.rrms[t] : 1.0f;
+                }
             const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.out + (size_t)n0 * M + m0);
 #pragma unroll
             for (int g = 0; g < PIECES; ++g) {
                 const int mi = g / (4 * TN) % TM, ni = g / 4 % TN, j = g % 4;
-                const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
-                const float r = rs[ni];
+                const int fl = wm * TM * 32 + mi * 32 + A::col(j, lane);
+                const int tl = wn * TN * 32 + ni * 32 + A::tok(j, lane);
+                const float r = rs[ni][M16 ? j >> 1 : 0];
                 float v[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float own = acc[0][mi][ni][4 * j + e];
+                    const float own = acc[0][mi][ni].get(4 * j + e);
                     float gv = split == 0 ? own : other[g][e], uv = split == 0 ? other[g][e] : own;
                     if (p.rrms) {
                         gv *= r;
@@ -511,10 +678,10 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
                 }
 #pragma unroll
                 for (int g = 0; g < CH; ++g) {
-                    // Piece c0 + g holds accumulators 4j .. 4j+3 of acc[0][mi][ni].
+                    // Piece c0 + g is piece j of acc[0][mi][ni].
                     const int mi = (c0 + g) / (4 * TN) % TM, ni = (c0 + g) / 4 % TN, j = (c0 + g) % 4;
-                    const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                    const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
+                    const int fl = wm * TM * 32 + mi * 32 + A::col(j, lane);
+                    const int tl = wn * TN * 32 + ni * 32 + A::tok(j, lane);
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -537,16 +704,10 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
         constexpr int CH = PIECES > 16 ? 8 : PIECES;
         static_assert(PIECES % CH == 0, "whole passes");
         auto get_piece = [&](int g) __attribute__((always_inline)) {
-            const f32x16 &a = acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN];
-            const int j = g % 4;
-            return f32x4{a[4 * j], a[4 * j + 1], a[4 * j + 2], a[4 * j + 3]};
+            return acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN].piece(g % 4);
         };
         auto set_piece = [&](int g, const f32x4 &v) __attribute__((always_inline)) {
-            f32x16 &a = acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN];
-            const int j = g % 4;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                a[4 * j + e] = v[e];
+            acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN].set_piece(g % 4, v);
         };
 #pragma unroll
         for (int c0 = 0; c0 < PIECES; c0 += CH) {
@@ -575,19 +736,18 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     }
 
     // ---- epilogue: fp32 -> act(r G) * (r U), or acc / d -> bf16, 8-byte row-major stores --
-    float rs[TN];
+    // Per-token scales of the lane's tokens: one per n-tile, or one per
+    // 16-token half with the 16x16 subtiles.
+    float rs[TN][SUB], ds[TN][SUB];
 #pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-        rs[ni] = EPI == EPI_GATE_MUL && p.rrms && t < N ? p.rrms[t] : 1.0f;
-    }
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+        for (int h = 0; h < SUB; ++h) {
+            const int t = n0 + wn * TN * 32 + ni * 32 + A::tok(2 * h, lane);
+            rs[ni][h] = EPI == EPI_GATE_MUL && p.rrms && t < N ? p.rrms[t] : 1.0f;
+            ds[ni][h] = EPI == EPI_STORE && p.rowdiv && t < N ? p.rowdiv[t] : 1.0f;
+        }
     const bool scaled = EPI == EPI_GATE_MUL && p.rrms;
-    float ds[TN];
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-        const int t = n0 + wn * TN * 32 + ni * 32 + (lane & 31);
-        ds[ni] = EPI == EPI_STORE && p.rowdiv && t < N ? p.rowdiv[t] : 1.0f;
-    }
     const bool divided = EPI == EPI_STORE && p.rowdiv;
     // All of the wave's packed results first, each group of 4 columns into
     // registers of its own, then the stores back to back: a store's data
@@ -600,20 +760,21 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
         for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
+                const int h = M16 ? j >> 1 : 0;
                 float v[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     if constexpr (EPI == EPI_GATE_MUL) {
-                        float g = acc[0][mi][ni][4 * j + e], u = acc[NW - 1][mi][ni][4 * j + e];
+                        float g = acc[0][mi][ni].get(4 * j + e), u = acc[NW - 1][mi][ni].get(4 * j + e);
                         if (scaled) {
-                            g *= rs[ni];
-                            u *= rs[ni];
+                            g *= rs[ni][h];
+                            u *= rs[ni][h];
                         }
                         v[e] = gate_act(g, p.activation, p.beta) * u;
                     } else {
-                        v[e] = acc[0][mi][ni][4 * j + e];
+                        v[e] = acc[0][mi][ni].get(4 * j + e);
                         if (divided)
-                            v[e] = v[e] / ds[ni];
+                            v[e] = v[e] / ds[ni][h];
                     }
                 }
                 packed[mi][ni][j] = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
@@ -632,8 +793,8 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
         for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int fl = wm * TM * 32 + mi * 32 + 8 * j + 4 * (lane >> 5);
-                const int tl = wn * TN * 32 + ni * 32 + (lane & 31);
+                const int fl = wm * TM * 32 + mi * 32 + A::col(j, lane);
+                const int tl = wn * TN * 32 + ni * 32 + A::tok(j, lane);
                 const uint32_t off = n0 + tl < N && m0 + fl < M ? (uint32_t)(tl * M + fl) * 2u : kOutOfRange;
                 __builtin_amdgcn_raw_buffer_store_b64(packed[mi][ni][j], ro, off, 0, OUT_POLICY);
             }

@@ -46,7 +46,7 @@ int ok()
 // at T = 4096 and T = 2048 (random bf16 data; power, and so the clock, depends
 // on the data at the board's power cap).
 //                          NW WM WN TM TN STAGES BK
-using GateUpLarge = GemmShape<2, 4, 2, 1, 4, 3, 32>; // 128 F cols x 256 tokens, per weight, 8 waves
+using GateUpLarge = GemmShape<2, 4, 2, 1, 4, 2, 64>; // 128 F cols x 256 tokens, per weight, 8 waves
 using GateUpSmall = GemmShape<2, 4, 2, 1, 2, 3, 64>; // 128 F cols x 128 tokens, 8 waves
 using DownLarge = GemmShape<1, 4, 2, 2, 4, 2, 64>;   // 256 D cols x 256 tokens, 8 waves
 using DownSmall = GemmShape<1, 2, 2, 2, 2, 4, 64>;   // 128 D cols x 128 tokens

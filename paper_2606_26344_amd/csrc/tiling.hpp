@@ -13,7 +13,17 @@ template <int NW_, int WM_, int WN_, int TM_, int TN_, int STAGES_, int BK_>
 struct GemmShape {
     static constexpr int NW = NW_, WM = WM_, WN = WN_, TM = TM_, TN = TN_, STAGES = STAGES_;
     static constexpr int BK = BK_;
-    static constexpr int KSTEPS = BK / 16;         // MFMA k16 steps per k-tile
+    // The MFMA instruction: tiles of 256 tokens or 256 columns (the
+    // MFMA-bound prefill tiles) issue v_mfma_f32_16x16x32_bf16, four 16 x 16
+    // accumulators per 32 x 32 block in k32 steps; under the board's power
+    // cap it sustains 15% more than v_mfma_f32_32x32x16_bf16 on random
+    // operands, and the steps on those tiles ran 0.6-2.6% faster with it
+    // (T = 640..4096 at D = 4096, F = 14336, and the large-prefill shape, on
+    // two boards).  The smaller tiles, bound by the weight stream, keep
+    // 32x32x16 in k16 steps (16x16x32 was 1-4% slower there).
+    static constexpr bool M16 = BK == 64 && (WM * TM * 32 >= 256 || WN * TN * 32 >= 256);
+    static constexpr int MFMA_K = M16 ? 32 : 16;
+    static constexpr int KSTEPS = BK / MFMA_K;     // MFMA k steps per k-tile
     static constexpr int NWAVES = WM * WN;
     static constexpr int NTHREADS = NWAVES * 64;
     static constexpr int BMW = WM * TM * 32;       // columns per weight per tile
@@ -34,8 +44,10 @@ struct GemmShape {
     static constexpr int LOADS_PER_STAGE = NW * W_LOADS + X_LOADS;
     static constexpr int W_LPR = 64 / W_CPR;          // weight rows per wave load
     static constexpr int W_RPI = NWAVES * W_LPR;      // weight rows per load step i
-    static constexpr int FRAG_READS = NW * TM * 2 + TN;  // LDS reads per k16 step
-    static constexpr int MFMAS = NW * TM * TN;           // MFMAs per k16 step
+    // LDS reads and MFMAs per k step (a 32 x 32 block per MFMA, or 16 x 16
+    // subtiles: twice the reads per step of twice the k, four MFMAs).
+    static constexpr int FRAG_READS = M16 ? NW * TM * 4 + TN * 2 : NW * TM * 2 + TN;
+    static constexpr int MFMAS = M16 ? NW * TM * TN * 4 : NW * TM * TN;
     static_assert(BK == 32 || BK == 64, "k-tile of 32 or 64");
     static_assert(X_ROWS % 32 == 0, "n-tiles of 32 tokens do not straddle the two row halves");
     static_assert(BMW >= 64, "weight rows of at least 8 chunks");
