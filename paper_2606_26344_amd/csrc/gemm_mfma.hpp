@@ -92,10 +92,11 @@ template <int CPR, bool M16>
 __device__ __forceinline__ int w_swizzle(int k)
 {
     if constexpr (CPR >= 16 && M16) {
-        // The 16x16x32 reads take rows k and k + 8 in one pass as well: the
-        // rows with bit 3 set use four other XOR values.
+        // The 16x16x32 reads take rows k and k + 16 in one pass as well
+        // (lane groups 0 and 1 read k groups 0 and 2): the rows with bit 4
+        // set use four other XOR values.
         const int g = k & 3;
-        if (k & 8)
+        if (k & 16)
             return g == 0 ? 2 : g == 1 ? 4 : g == 2 ? 8 : 14;
         return g == 0 ? 0 : g == 1 ? 6 : g == 2 ? 10 : 12;
     } else if constexpr (CPR >= 16) {
@@ -240,17 +241,18 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     // ---- staging addresses ---------------------------------------------------
     // Weight load i of this lane: row i*W_RPI + w_k, physical chunk lane %
     // W_CPR holding the logical chunk that the row's swizzle maps there.  The
-    // swizzle depends on the row only through bits 0, 1 and 3; bits 0 and 1
-    // are the same for every i, bit 3 too unless W_RPI = 8 (then it
-    // alternates), so one or two voffsets serve all i and the row step goes
-    // into the scalar offset.
+    // swizzle depends on the row only through bits 0, 1 and 4; bits 0 and 1
+    // are the same for every i, and bit 4 of w_k + i*W_RPI flips with bit 4
+    // of i*W_RPI, so two voffsets serve all i and the row step goes into the
+    // scalar offset.
     const int w_k = wave * S::W_LPR + lane / S::W_CPR;
     auto w_voff_of = [&](int row) __attribute__((always_inline)) {
         const int c = (lane % S::W_CPR) ^ w_swizzle<S::W_CPR, S::M16>(row);
         return m0 + c * 8 < M ? (uint32_t)(w_k * M + c * 8) * 2u : kOutOfRange;
     };
-    const uint32_t w_voff = w_voff_of(w_k), w_voff_b3 = w_voff_of(w_k ^ 8);
-    static_assert(S::W_RPI % 16 == 0 || S::W_RPI == 8, "row bits 0, 1 fixed across loads, bit 3 fixed or alternating");
+    const uint32_t w_voff = w_voff_of(w_k), w_voff_b4 = w_voff_of(w_k ^ 16);
+    static_assert(S::W_RPI % 4 == 0 && S::W_RPI >= 4, "row bits 0, 1 fixed across loads");
+    static_assert(S::W_RPI >= 16 || (16 % S::W_RPI == 0), "bit 4 of w_k + i*W_RPI is that of w_k xor i*W_RPI");
     const uint32_t w_soff_step = (uint32_t)S::W_RPI * (uint32_t)M * 2u;
     // Activation load i: LDS row x_r(i) (8 rows per wave load), physical
     // chunk lane % 8 holding chunk x_c of token x_t.  Tokens past N are
@@ -283,9 +285,9 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             const __amdgpu_buffer_rsrc_t rw = make_rsrc((w == 0 ? w_first : p.w1) + (size_t)k0 * M + m0);
 #pragma unroll
             for (int i = 0; i < S::W_LOADS; ++i) {
-                const uint32_t v = (masked && i * S::W_RPI + w_k >= krem)      ? kOutOfRange
-                                   : (S::W_RPI == 8 && (i & 1)) ? w_voff_b3
-                                                                 : w_voff;
+                const uint32_t v = (masked && i * S::W_RPI + w_k >= krem) ? kOutOfRange
+                                   : ((i * S::W_RPI) & 16)                  ? w_voff_b4
+                                                                            : w_voff;
                 uint8_t *dst = sbuf + w * S::W_TILE_BYTES + (i * NWAVES + wave) * 1024;
                 if constexpr (STREAM_W)
                     load16_to_lds_stream(rw, dst, v, (uint32_t)i * w_soff_step);
@@ -310,12 +312,16 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     // column chunk c; each 16-lane group reads 4 rows x 16 columns, the two
     // groups of a half-wave the two 16-column halves, the two half-waves k
     // rows 0..7 and 8..15.  16x16x32: the 16-column half sa of m-tile mi for
-    // k32 step kk: the four 16-lane groups read k rows 8g .. 8g+7 of the
-    // same 16 columns.
+    // k32 step kk: the four 16-lane groups g read k rows 8 kg(g) .. +7 of the
+    // same 16 columns, kg = 0, 2, 1, 3 for g = 0, 1, 2, 3 (any order of the
+    // four k groups gives the same sums if A and B share it; this one keeps
+    // the lanes l and l + 32 that the LDS serves together on neighbouring
+    // chunks of a token row, as the 32x32x16 layout does).
     constexpr bool M16 = S::M16;
     constexpr int SUB = M16 ? 2 : 1; // 16-wide halves of a 32-wide block per fragment
     using A = AccBlock<M16>;
-    const int r_lane = M16 ? 8 * (lane >> 4) + ((lane & 15) >> 2) : 8 * (lane >> 5) + ((lane & 15) >> 2);
+    const int kg = ((lane >> 4) & 1) << 1 | (lane >> 5); // k group of a 16x16x32 lane group
+    const int r_lane = M16 ? 8 * kg + ((lane & 15) >> 2) : 8 * (lane >> 5) + ((lane & 15) >> 2);
     int a_off[TM][SUB];
 #pragma unroll
     for (int mi = 0; mi < TM; ++mi)
@@ -329,7 +335,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     // t % X_ROWS, combined chunk 2*kk + lane/32 + X_CPT * (t / X_ROWS); the
     // chunk bits of the byte address are XORed with 32*kk for step kk.
     // 16x16x32: half sb of n-tile ni, token t = wn*TN*32 + ni*32 + 16 sb +
-    // lane%16, chunk 4*kk + lane/16 (XOR 64*kk).
+    // lane%16, chunk 4*kk + kg (XOR 64*kk).
     int b_off[TN][SUB];
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni)
@@ -337,7 +343,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
         for (int sb = 0; sb < SUB; ++sb) {
             const int t = wn * TN * 32 + ni * 32 + (M16 ? 16 * sb + (lane & 15) : lane & 31);
             const int r = t % S::X_ROWS;
-            const int cc = (M16 ? lane >> 4 : lane >> 5) + S::X_CPT * (t / S::X_ROWS);
+            const int cc = (M16 ? kg : lane >> 5) + S::X_CPT * (t / S::X_ROWS);
             b_off[ni][sb] = r * 128 + ((cc ^ x_swizzle(r)) << 4);
         }
 
