@@ -41,12 +41,14 @@ value in TFLOP/s of 2MKN, the matmul kernel as the dominant one.
 --path picks the kernel path (auto, gemv, mfma, or fused: the one-kernel
 decode path); --graph adds the step's time when captured in a HIP graph and
 replayed; --vendor-gemm adds the vendor library's time for the same matmul
-shapes (context).  The default run also times, after the workloads, a loop of
-MFMAs on register operands (paper_2606_26344_amd/mfma_ceiling, random and
-all-zero data): under the board's power limit the random-data rate is the
-ceiling of any GEMM on random data, reported beside the MFMA-bound records
-as roofline.power_capped_mfma (--mfma-ceiling prints it alone).  Only one
-GPU is used: --gpus above 1 exits with a message.
+shapes (context).  The default run also times, after the workloads, loops of
+MFMAs on register operands (paper_2606_26344_amd/mfma_ceiling, 32x32x16 and
+16x16x32, random and all-zero data): under the board's power limit the
+random-data rate of an instruction is the ceiling of any GEMM on random data
+that issues it, reported beside the MFMA-bound records as
+roofline.power_capped_mfma, with the fraction of the dominant kernel's own
+instruction (--mfma-ceiling prints the ceilings alone).  Only one GPU is
+used: --gpus above 1 exits with a message.
 """
 from __future__ import annotations
 
@@ -958,6 +960,17 @@ def mfma_ceiling(ms=20.0):
     return out
 
 
+def mfma_instruction(kernel):
+    """The MFMA instruction a gemm_mfma_kernel<GemmShape<NW, WM, WN, TM, TN,
+    STAGES, BK>> issues: v_mfma_f32_16x16x32_bf16 where its tile has 256
+    columns (WM TM 32) or 256 tokens (WN TN 32) and 64-row k-tiles, else
+    v_mfma_f32_32x32x16_bf16."""
+    if "GemmShape<" not in kernel:
+        return "32x32x16"
+    nw, wm, wn, tm, tn, stages, bk = [int(v) for v in kernel.split("GemmShape<")[1].split(">")[0].split(",")[:7]]
+    return "16x16x32" if bk == 64 and (wm * tm * 32 >= 256 or wn * tn * 32 >= 256) else "32x32x16"
+
+
 def run_suite(args):
     """The default benchmark: one JSON line whose value is the decode
     workload's (T = 1, the configuration the HBM half of the metric is quoted
@@ -993,9 +1006,13 @@ def run_suite(args):
     for rec in configs.values():
         if rec["roofline"]["bound"] == "mfma":
             ctx = dict(ceiling)
-            if "random_data_tflops" in ceiling:
-                ctx["frac_of_random_data_ceiling"] = round(
-                    rec["roofline"]["achieved"] / ceiling["random_data_tflops"], 4)
+            # The dominant kernel's own instruction: 16x16x32 for the tiles
+            # of 256 tokens or 256 columns, else 32x32x16.
+            instr = mfma_instruction(rec["roofline"].get("kernel", ""))
+            ctx["kernel_mfma"] = instr
+            key = "random_data_tflops" + ("" if instr == "32x32x16" else "_" + instr)
+            if key in ceiling:
+                ctx["frac_of_random_data_ceiling"] = round(rec["roofline"]["achieved"] / ceiling[key], 4)
             rec["roofline"]["power_capped_mfma"] = ctx
     result["config"]["suite"] = [SUITE_HEADLINE] + list(configs)
     result["configs"] = configs

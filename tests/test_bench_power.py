@@ -39,3 +39,10 @@ def test_mfma_ceiling_reads_the_program_output(tmp_path, monkeypatch):
     assert got["random_data_tflops_16x16x32"] == 2090.0 and got["zero_data_tflops_16x16x32"] == 2470.0
     monkeypatch.setattr(bench, "MFMA_CEILING", str(tmp_path / "missing"))
     assert "error" in bench.mfma_ceiling()
+
+
+def test_mfma_instruction_of_a_kernel_name():
+    assert bench.mfma_instruction("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4, 2, 64>, 0, false, false>") == "16x16x32"
+    assert bench.mfma_instruction("gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 2, 3, 64>, 1, true, false>") == "16x16x32"
+    assert bench.mfma_instruction("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 2, 3, 64>, 0, true, true>") == "32x32x16"
+    assert bench.mfma_instruction("gemv_splitk_kernel<1, 2, 0, false>") == "32x32x16"
