@@ -102,7 +102,7 @@ __device__ __forceinline__ bool gemv_item(const GemvParams &p, int item, GemvSha
     static_assert(!RMS || EPI == EPI_GATE_MUL, "RMSNorm belongs to the gate/up step");
     using L = GemvLayout<NT, NW>;
     constexpr int RG = L::RG; // row groups per block
-    constexpr int U = gemv_batch_rows<NT>();
+    constexpr int U = gemv_batch_rows<NT, NW>();
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int strip = item % p.strips;
     const int split = item / p.strips;

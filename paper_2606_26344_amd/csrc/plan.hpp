@@ -14,6 +14,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 
 #include "gmlp.h"
 #include "softmax_matmul.h"
@@ -300,15 +301,19 @@ void pair_step(Step &s, int M, int N, int K, int group_m)
 int gemv_batch_span(int nt, int nw)
 {
     const int rg = gemv_threads(nt) / gemv_strip_lanes(nt, nw);
+    auto rows = [nw](auto ntc) {
+        constexpr int NT = decltype(ntc)::value;
+        return nw == 2 ? gemv_batch_rows<NT, 2>() : gemv_batch_rows<NT, 1>();
+    };
     switch (nt) {
-    case 1: return rg * gemv_batch_rows<1>();
-    case 2: return rg * gemv_batch_rows<2>();
-    case 3: return rg * gemv_batch_rows<3>();
-    case 4: return rg * gemv_batch_rows<4>();
-    case 5: return rg * gemv_batch_rows<5>();
-    case 6: return rg * gemv_batch_rows<6>();
-    case 7: return rg * gemv_batch_rows<7>();
-    default: return rg * gemv_batch_rows<8>();
+    case 1: return rg * rows(std::integral_constant<int, 1>{});
+    case 2: return rg * rows(std::integral_constant<int, 2>{});
+    case 3: return rg * rows(std::integral_constant<int, 3>{});
+    case 4: return rg * rows(std::integral_constant<int, 4>{});
+    case 5: return rg * rows(std::integral_constant<int, 5>{});
+    case 6: return rg * rows(std::integral_constant<int, 6>{});
+    case 7: return rg * rows(std::integral_constant<int, 7>{});
+    default: return rg * rows(std::integral_constant<int, 8>{});
     }
 }
 

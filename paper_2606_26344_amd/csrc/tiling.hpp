@@ -88,9 +88,13 @@ constexpr int gemv_strip_lanes(int nt, int nw) { return nt <= kGemvWideTokens &&
 // Weight rows per lane per load batch (U), and batches in flight per lane
 // (DEPTH): DEPTH*NW*U loads of 16 bytes in flight per lane, within the
 // register budget of NT tokens (with the 512-thread blocks, 128 KB in flight
-// per block at U = 4).
-template <int NT>
-constexpr int gemv_batch_rows() { return NT <= 6 ? 4 : 2; }
+// per block at U = 4 for the gate/up step).  The down step's 8-wave blocks
+// (up to kGemvWideTokens tokens) do best with less in flight: U = 2, i.e.
+// 32 KB per block (measured at D = 4096, F = 14336: down 20.4 -> 19.9 us at
+// T = 1, 20.9 -> 20.6 at T = 2; U = 2 for the 4-wave blocks of T = 3..5 was
+// 25-29% slower, and a third batch in flight at U = 4 made T = 1 23.6 us).
+template <int NT, int NW>
+constexpr int gemv_batch_rows() { return NW == 1 && NT <= kGemvWideTokens ? 2 : NT <= 6 ? 4 : 2; }
 template <int NT>
 constexpr int gemv_depth() { return 2; }
 
