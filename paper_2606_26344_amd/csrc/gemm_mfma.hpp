@@ -617,7 +617,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             // This block's accumulators are G (split 0) or U (split 1); the
             // other block's are read back piece by piece, and every piece
             // gives 4 columns of H at once.
-            static_assert(PIECES <= 16, "the other block's pieces are read in one pass");
+            static_assert(PIECES <= 24, "the other block's pieces are read in one pass");
             const uint32_t obase = wave_base(1 - split);
             f32x4 other[PIECES];
 #pragma unroll

@@ -193,7 +193,9 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
                         s.splits, s.tiles_n);
         if (s.N <= PairMid96::BN)
             return launch_gemm<PairMid96, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
-        return launch_gemm<PairSmall, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        if (s.N <= PairSmall::BN)
+            return launch_gemm<PairSmall, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        return launch_gemm<PairMid192, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)
                      : launch_gemv<2, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, st);

@@ -73,10 +73,12 @@ using DownMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>;   // 128 D cols x 96 tokens, 
 using FusedDownTiny = GemmShape<1, 4, 1, 1, 1, 4, 64>;
 using FusedDownMid = GemmShape<1, 4, 1, 1, 2, 4, 64>;
 // The paired gate/up tiles (one weight per block, a G and a U block per
-// column tile, EPI_GATE_PAIR) for one token tile of 65 to 128 tokens: the
-// down step's tiles (with 3 stages at 128 tokens: 0.3 us faster than 4).
+// column tile, EPI_GATE_PAIR) for one token tile of 65 to 192 tokens: the
+// down step's tiles (with 3 stages at 128 tokens: 0.3 us faster than 4), and
+// a 192-token tile.
 using PairMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>; // 128 F cols x 96 tokens, 4 waves
 using PairSmall = GemmShape<1, 2, 2, 2, 2, 3, 64>; // 128 F cols x 128 tokens, 4 waves
+using PairMid192 = GemmShape<1, 4, 1, 1, 6, 3, 64>; // 128 F cols x 192 tokens, 4 waves
 // Column tiles swept per token tile by consecutive blocks (L2 locality),
 // from a sweep at T=4096/2048 on MI355X.
 constexpr int kGroupGateUp = 8;
@@ -260,7 +262,8 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
 
 // The paired gate/up step (EPI_GATE_PAIR): one-weight tiles, a G and a U
 // block per column tile, each over the whole of K.  It replaces a dual-B
-// plan that splits K in two where that plan's blocks fill more than three
+// plan of one token tile that splits K in two (and, below, one of two
+// 128-token tiles) where that plan's blocks fill more than three
 // quarters of the chip: the same blocks and weight bytes, half the fp32
 // exchange and 256-byte row segments of one weight per block, but each
 // block stages all of X rather than half.  Measured at D = 4096 over
@@ -415,6 +418,16 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         else
             pair_step<PairSmall>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
     }
+    // 129 to 192 tokens, where the dual-B plan runs two 128-token tiles
+    // without split-K on as many blocks: one 192-token tile as pairs, each
+    // weight element read once (the weights streamed) and X staged 1.5x
+    // instead of twice per column tile.  Measured at D = 4096, F = 14336,
+    // gate/up alone: T = 129 68.5 -> 67.4 us, 160 70.9 -> 68.4, 192 74.3 ->
+    // 68.6-68.8; pairs of 256-token tiles for T = 193..256 were slower (T =
+    // 224: 77.7 -> 89-91 us).
+    if (p.gate_up.kind == K_GEMM_GU_S && p.gate_up.tiles_n == 2 && p.gate_up.splits == 1 && T <= PairMid192::BN &&
+        p.gate_up.blocks >= kPairMinBlocks && p.gate_up.blocks <= kBlockTarget)
+        pair_step<PairMid192>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
     // Down: large tiles once there are enough of them to fill the chip.
     // Above one token tile, from 40 of them up to a round, large tiles split over K to fill one
     // round beat two rounds of 128 x 128 tiles (measured: D = 4096, F = 14336
@@ -643,7 +656,9 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_GU_W: return "gemm_mfma_kernel<" + shape_name<GateUpMid96>() + ", 0, true, true>";
     case K_GEMM_DN_W: return "gemm_mfma_kernel<" + shape_name<DownMid96>() + ", 1, true, true>";
     case K_GEMM_GU_P: {
-        const std::string shape = s.N <= PairMid96::BN ? shape_name<PairMid96>() : shape_name<PairSmall>();
+        const std::string shape = s.N <= PairMid96::BN   ? shape_name<PairMid96>()
+                                  : s.N <= PairSmall::BN ? shape_name<PairSmall>()
+                                                         : shape_name<PairMid192>();
         return "gemm_mfma_kernel<" + shape + ", 2, true, true>";
     }
     case K_GEMV:

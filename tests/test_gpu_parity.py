@@ -158,12 +158,14 @@ def test_eight_wave_gemv_strips(orc, T, D, F):
     _run(T, D, F, seed=3 * T + D + F, orc=orc)
 
 
-# 65 to 128 tokens where the dual-B gate/up tiles would split K in two over
-# more than 3/4 of the chip: a G and a U block per column tile, each over
-# the whole of K, the later of the two combining both into H.  96- and
-# 128-token tiles, K tails (D not a multiple of 64), last column tiles cut
-# short by F (F = 12424, 14344, 12296), the fewest (97) and most (128) pairs.
-PAIRED = [(65, 264, 12800), (96, 4104, 12424), (97, 264, 16384), (128, 1032, 14344), (112, 520, 12296)]
+# 65 to 192 tokens where the dual-B gate/up tiles would split K in two (or
+# run two 128-token tiles) over more than 3/4 of the chip: a G and a U block
+# per column tile, each over the whole of K, the later of the two combining
+# both into H.  96-, 128- and 192-token tiles, K tails (D not a multiple of
+# 64), last column tiles cut short by F (F = 12424, 14344, 12296), the
+# fewest (97) and most (128) pairs.
+PAIRED = [(65, 264, 12800), (96, 4104, 12424), (97, 264, 16384), (128, 1032, 14344), (112, 520, 12296),
+          (129, 264, 14344), (160, 1032, 16384), (192, 520, 12424)]
 
 
 @pytest.mark.parametrize("T,D,F", PAIRED, ids=["T%dD%dF%d" % s for s in PAIRED])

@@ -54,11 +54,12 @@ def test_variant_ragged_shapes(orc, name, T, D, F):
 
 
 @pytest.mark.parametrize("name", sorted(VARIANTS))
-def test_variant_paired_gate_up_blocks(orc, name):
-    # 100 tokens, 97 column tiles of F: the G and U blocks of a pair
+@pytest.mark.parametrize("T", [100, 150])
+def test_variant_paired_gate_up_blocks(orc, name, T):
+    # 100 and 150 tokens, 97 column tiles of F: the G and U blocks of a pair
     # (activation and RMSNorm scale applied by the later one).
-    assert gmlp.describe(100, 520, 12296)[0][0].endswith(", 2, true, true>")
-    _run(orc, 100, 520, 12296, VARIANTS[name], seed=77, x_scale=3.0)
+    assert gmlp.describe(T, 520, 12296)[0][0].endswith(", 2, true, true>")
+    _run(orc, T, 520, 12296, VARIANTS[name], seed=77 + T, x_scale=3.0)
 
 
 @pytest.mark.parametrize("name", sorted(VARIANTS))
