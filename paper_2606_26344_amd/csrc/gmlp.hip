@@ -234,6 +234,8 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
                                                                                 nullptr, rowdiv, st);
     case K_GEMM_DN_X:
         return launch_gemm<DownWide, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
+    case K_GEMM_DN_Y: // one token tile: always streamed
+        return launch_gemm<DownMid192, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMM_DN_W: // one token tile: always streamed
         return launch_gemm<DownMid96, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);
