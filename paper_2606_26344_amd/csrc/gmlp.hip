@@ -185,6 +185,8 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     case K_GEMM_GU_M:
         return stream_weights(s) ? launch_gemm<GateUpMid, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
                                  : launch_gemm<GateUpMid, EPI_GATE_MUL, true, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+    case K_GEMM_GU_Y:
+        return launch_gemm<GateUp192, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_W: // one token tile: always streamed
         return launch_gemm<GateUpMid96, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMM_GU_P: // one token tile, a G and a U block per column tile
@@ -234,8 +236,11 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
                                                                                 nullptr, rowdiv, st);
     case K_GEMM_DN_X:
         return launch_gemm<DownWide, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
-    case K_GEMM_DN_Y: // one token tile: always streamed
-        return launch_gemm<DownMid192, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
+    case K_GEMM_DN_Y:
+        return stream_weights(s) ? launch_gemm<DownMid192, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                                  nullptr, rowdiv, st)
+                                 : launch_gemm<DownMid192, EPI_STORE, true, false>(s, Wd, nullptr, H, Y, ws, l, plain,
+                                                                                   nullptr, rowdiv, st);
     case K_GEMM_DN_W: // one token tile: always streamed
         return launch_gemm<DownMid96, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMV: return launch_gemv<1, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, st, rowdiv);

@@ -80,6 +80,10 @@ using FusedDownMid = GemmShape<1, 4, 1, 1, 2, 4, 64>;
 using PairMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>; // 128 F cols x 96 tokens, 4 waves
 using PairSmall = GemmShape<1, 2, 2, 2, 2, 3, 64>; // 128 F cols x 128 tokens, 4 waves
 using PairMid192 = GemmShape<1, 4, 1, 1, 6, 3, 64>; // 128 F cols x 192 tokens, 4 waves
+// 257 to 384 tokens: two 192-token tiles (a quarter less work and
+// activation staging than two 256-token tiles at T = 384, a quarter more at
+// T = 257 than needed instead of twice).
+using GateUp192 = GemmShape<2, 4, 1, 1, 6, 4, 32>; // 128 F cols x 192 tokens, per weight, 4 waves
 // Column tiles swept per token tile by consecutive blocks (L2 locality),
 // from a sweep at T=4096/2048 on MI355X.
 constexpr int kGroupGateUp = 8;
@@ -131,7 +135,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 enum Kind {
     K_NONE,
-    K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T, K_GEMM_GU_P,
+    K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T, K_GEMM_GU_P, K_GEMM_GU_Y,
     K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMM_DN_X, K_GEMM_DN_Y,
     K_GEMV
 };
@@ -156,6 +160,7 @@ struct Step {
     // of the chip.
     int tile_base = 0, tile_count = 0;
     int tail_tiles = 0, tail_splits = 1, tail_k_split = 0;
+    int64_t block_macs = 0; // GEMM: multiply-adds of one block of the main launch
 };
 
 // The second launch of a step with a tail: its last tail_tiles tiles, split
@@ -252,6 +257,7 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
         }
     }
     s.blocks = s.tile_count * s.splits;
+    s.block_macs = (int64_t)S::BMW * S::BN * nw * s.k_split;
     s.threads = S::NTHREADS;
     s.counters = std::max(s.splits > 1 ? tiles : 0, s.tail_tiles);
     // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane];
@@ -402,7 +408,14 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     // leave (measured at D = 4096, F = 14336: T = 320, 384 11% faster,
     // T = 512 and 1024 8%).
     const int64_t large_tiles = cdiv(T, GateUpLarge::BN) * cdiv(F, GateUpLarge::BMW);
-    if (large_tiles >= 512 || (T > 256 && large_tiles >= 192))
+    // Two 192-token tiles where they make one round that is at least three
+    // quarters full (measured at D = 4096, F = 14336 against two 256-token
+    // tiles, gate/up: T = 257 111.8 -> 89.0 us, 320 114.2 -> 93.5, 384
+    // 115.8 -> 98.3; 8 waves with 64-row k-tiles were 6-11% slower).
+    const int64_t tiles192 = cdiv(T, GateUp192::BN) * cdiv(F, GateUp192::BMW);
+    if (T > 256 && T <= 2 * GateUp192::BN && tiles192 <= kBlockTarget && tiles192 >= kBlockTarget * 3 / 4)
+        gemm_step<GateUp192>(p.gate_up, K_GEMM_GU_Y, (int)F, (int)T, (int)D, 2, false, kGroupGateUp);
+    else if (large_tiles >= 512 || (T > 256 && large_tiles >= 192))
         gemm_step<GateUpLarge>(p.gate_up, K_GEMM_GU_L, (int)F, (int)T, (int)D, 2, false, kGroupGateUp);
     else if (T <= GateUpTiny::BN)
         gemm_step<GateUpTiny>(p.gate_up, K_GEMM_GU_T, (int)F, (int)T, (int)D, 2, true, kGroupGateUp);
@@ -474,6 +487,21 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         gemm_step<DownMid192>(p.down, K_GEMM_DN_Y, (int)D, (int)T, (int)F, 1, true, kGroupDown);
     else
         gemm_step<DownSmall>(p.down, K_GEMM_DN_S, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+    // 257 to 384 tokens: two 192-token down tiles split over K where there
+    // are 64 to 128 of them (so that at least two splits fill a round) and
+    // a block's work is at most 95% of what the rules above give it.
+    // Measured: down at D = 4096, F = 14336 T = 257 61.9 -> 58.7 us, 320
+    // 62.4 -> 59.9, 384 62.9 -> 60.4 (93% of the work); D = 8192, F = 28672,
+    // T = 320 221.9 -> 195.0 (75%); slower at equal work (D = 5120,
+    // F = 13824, T = 300: 69.5 -> 74.7) and with 32 tiles (D = 2048,
+    // F = 8192, T = 300: 27.5 -> 34.4).
+    const int64_t down192 = cdiv(T, DownMid192::BN) * cdiv(D, DownMid192::BMW);
+    if (T > 256 && T <= 2 * DownMid192::BN && down192 >= 64 && down192 <= kBlockTarget / 2) {
+        Step mid;
+        gemm_step<DownMid192>(mid, K_GEMM_DN_Y, (int)D, (int)T, (int)F, 1, true, kGroupDown);
+        if (p.down.tail_tiles == 0 && p.down.blocks <= kBlockTarget && mid.block_macs * 20 <= p.down.block_macs * 19)
+            p.down = mid;
+    }
     return p;
 }
 
@@ -661,8 +689,10 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_DN_M:
         return "gemm_mfma_kernel<" + shape_name<DownMid>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_W: return "gemm_mfma_kernel<" + shape_name<GateUpMid96>() + ", 0, true, true>";
+    case K_GEMM_GU_Y: return "gemm_mfma_kernel<" + shape_name<GateUp192>() + ", 0, false, false>";
     case K_GEMM_DN_W: return "gemm_mfma_kernel<" + shape_name<DownMid96>() + ", 1, true, true>";
-    case K_GEMM_DN_Y: return "gemm_mfma_kernel<" + shape_name<DownMid192>() + ", 1, true, true>";
+    case K_GEMM_DN_Y:
+        return "gemm_mfma_kernel<" + shape_name<DownMid192>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_P: {
         const std::string shape = s.N <= PairMid96::BN   ? shape_name<PairMid96>()
                                   : s.N <= PairSmall::BN ? shape_name<PairSmall>()

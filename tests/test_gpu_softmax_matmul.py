@@ -116,11 +116,19 @@ def test_matmul_tail_tiles_split_over_k(sorc):
 
 
 def test_matmul_on_wide_tiles_split_over_k(sorc):
-    # 3 x 17 = 51 tiles of 256 x 128, 5 splits of 52 k-tiles: the divide by
-    # the softmax sums in the split-K epilogue of the wide tiles.
-    M, K, N = 384, 16384, 4104
+    # 2 x 17 = 34 tiles of 256 x 128 (a ragged second row tile), 3 splits:
+    # the divide by the softmax sums in the split-K epilogue of the wide
+    # tiles.
+    M, K, N = 448, 16384, 4104
     assert smm.describe(M, K, N)[-1][0] == "gemm_mfma_kernel<GemmShape<1, 4, 2, 2, 2, 3, 64>, 1, true, false>"
     _run(sorc, M, K, N, seed=43, rows=I.sample_rows(M, 24))
+
+
+def test_matmul_on_192_row_tiles_split_over_k(sorc):
+    # 257 to 384 rows: two 192-row tiles split over K, the second ragged.
+    M, K, N = 300, 16384, 4040
+    assert smm.describe(M, K, N)[-1][0] == "gemm_mfma_kernel<GemmShape<1, 4, 1, 1, 6, 3, 64>, 1, true, false>"
+    _run(sorc, M, K, N, seed=44, rows=I.sample_rows(M, 24))
 
 
 def test_probabilities_past_2_gib(sorc):

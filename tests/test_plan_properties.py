@@ -103,6 +103,28 @@ def test_gated_mlp_plan_covers_the_problem(T, D, F):
     assert ws % 256 == 0
 
 
+@pytest.mark.parametrize("T", [256, 257, 300, 320, 383, 384, 385])
+@pytest.mark.parametrize("D, F", [(4096, 14336), (8192, 28672), (8200, 16384), (1024, 4096), (2048, 14336)])
+def test_192_token_tiles_from_257_to_384_tokens(T, D, F):
+    """257 to 384 tokens run as two 192-token tiles: the gate/up step where
+    its tiles fill between 3/4 of a round and one round of 256 blocks, the
+    down step only where it has 64 to 128 tiles (two or more splits fill a
+    round), and at the model dimensions; each weight is then read by both
+    token tiles, so neither step streams it."""
+    (_, gu), (_, dn) = _steps(gmlp.describe(T, D, F))
+    in_range = 256 < T <= 384
+    gu_tiles = _cdiv(F, 128) * _cdiv(T, 192)
+    dn_tiles = _cdiv(D, 128) * _cdiv(T, 192)
+    assert (_tile(gu[0][0]) == (128, 192)) == (in_range and 192 <= gu_tiles <= 256)
+    if _tile(dn[0][0]) == (128, 192):
+        assert 128 < T <= 192 or (in_range and 64 <= dn_tiles <= 128)
+    if in_range and (D, F) in ((4096, 14336), (8192, 28672)):
+        assert _tile(dn[0][0]) == (128, 192)
+    for name, _, _, _ in gu + dn:
+        if _tile(name) == (128, 192) and in_range:
+            assert not _flags(name)[2]
+
+
 @settings(max_examples=100, deadline=None)
 @given(T=st.integers(min_value=1, max_value=8), D=dims, F=dims)
 def test_fused_plan_is_the_gemv_items(T, D, F):
