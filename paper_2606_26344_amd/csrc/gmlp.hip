@@ -205,6 +205,18 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     }
 }
 
+// The gate/up step of a plan: on a token split, the rest rows follow as a
+// problem of their own, at offset rows of X and H.
+int run_gate_up_plan(const Plan &p, const void *X, const void *Wg, const void *Wu, void *H, int64_t D,
+                     int64_t F, uint8_t *ws, const Layout &l, const Variant &v, hipStream_t st)
+{
+    int rc = run_gate_up(p.gate_up, X, Wg, Wu, H, ws, l, v, st);
+    if (rc || !p.rest_row)
+        return rc;
+    return run_gate_up(p.gate_up_rest, static_cast<const uint16_t *>(X) + p.rest_row * D, Wg, Wu,
+                       static_cast<uint16_t *>(H) + p.rest_row * F, ws, l, v, st);
+}
+
 // The down step, Y = bf16(H Wd), or with row divisors d, Y = bf16((H Wd) / d)
 // row by row (the divide of Softmax+MatMul moved past its matmul).
 int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws, const Layout &l,
@@ -408,8 +420,10 @@ int gmlp_describe(int64_t T, int64_t D, int64_t F, int path, char *buf, size_t b
         snprintf(buf, bytes, "%s", text.c_str());
         return ok();
     }
-    for (const Step *s : {&plan.gate_up, &plan.down})
-        text += describe_step(*s, s == &plan.gate_up);
+    text += describe_step(plan.gate_up, true);
+    if (plan.rest_row)
+        text += describe_step(plan.gate_up_rest, true);
+    text += describe_step(plan.down, false);
     snprintf(buf, bytes, "%s", text.c_str());
     return ok();
 }
@@ -483,7 +497,7 @@ int gmlp_forward_variant(const void *X, const void *Wg, const void *Wu, const vo
         return rc ? rc : ok();
     }
     void *H = ws + l.h_off;
-    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, ws, l, v, st)) ||
+    if ((rc = run_gate_up_plan(plan, X, Wg, Wu, H, D, F, ws, l, v, st)) ||
         (rc = run_down(plan.down, H, Wd, Y, ws, l, st)))
         return rc;
     return ok();
@@ -609,8 +623,8 @@ int gmlp_gate_up_variant(const void *X, const void *Wg, const void *Wu, void *H,
     if ((rc = check_workspace(workspace, ws_bytes, l)))
         return rc;
     const Plan plan = make_plan(T, D, F, path);
-    if ((rc = run_gate_up(plan.gate_up, X, Wg, Wu, H, static_cast<uint8_t *>(workspace), l, v,
-                          static_cast<hipStream_t>(stream))))
+    if ((rc = run_gate_up_plan(plan, X, Wg, Wu, H, D, F, static_cast<uint8_t *>(workspace), l, v,
+                               static_cast<hipStream_t>(stream))))
         return rc;
     return ok();
 }

@@ -180,6 +180,10 @@ Step tail_step(const Step &s)
 struct Plan {
     int path = GMLP_PATH_AUTO;
     Step gate_up, down;
+    // Gate/up on a token split: gate_up covers rows [0, rest_row), and
+    // gate_up_rest, planned as a problem of its own, rows [rest_row, T).
+    int64_t rest_row = 0;
+    Step gate_up_rest;
 };
 
 
@@ -370,6 +374,7 @@ void gemv_step(Step &s, int M, int N, int K, int nw)
 Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
 {
     Plan p;
+    const int asked = path;
     if (path == GMLP_PATH_AUTO)
         path = T <= kGemvAutoTokens ? GMLP_PATH_GEMV : GMLP_PATH_MFMA;
     p.path = path;
@@ -502,6 +507,35 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
         if (p.down.tail_tiles == 0 && p.down.blocks <= kBlockTarget && mid.block_macs * 20 <= p.down.block_macs * 19)
             p.down = mid;
     }
+    // From 513 tokens, where the 256-token gate/up tiles leave a last round
+    // of split-K tail tiles and the last token tile is at most half full,
+    // its r tokens may run as a gate/up problem of their own after the
+    // whole 256-token tiles (few-token tiles that stream the weights,
+    // mostly from the last-level cache) instead of padding them to 256
+    // tokens.  The choice follows a cost in rounds of full-K tiles fitted
+    // to measurements: a partial round costs a round, a tail launch split s
+    // ways 1/s + 0.27, the r-token problem 0.9 C / 256 for C column tiles
+    // (it streams weights that a round of tiles reads in about 280 tiles'
+    // time).  Gate/up at D = 4096, F = 14336: T = 520 176.0 -> 148.9 us,
+    // 640 178.0 -> 155.6, 1088 277.0 -> 252.5, 1600 364.8 -> 347.1, 2340
+    // 490.2 -> 467.0, 2880 578.0 -> 562.8, kept whole at 1800 (388.7, split
+    // 407.4); at D = 8192, F = 28672: T = 1100 1004.9 -> 932.5, 1600 1380.4
+    // -> 1329.3, kept whole at 800 (762.2, split 797.6).  The down step
+    // keeps one plan: splitting it was slower at every measured T.
+    const int64_t rest = T % GateUpLarge::BN;
+    if (p.gate_up.kind == K_GEMM_GU_L && rest > 0 && rest <= GateUpLarge::BN / 2 && T > 2 * GateUpLarge::BN) {
+        const auto rounds_milli = [](const Step &s) {
+            const int64_t full = s.tile_count / kBlockTarget, part = s.tile_count % kBlockTarget;
+            return 1000 * (full + (part ? 1 : 0)) + (s.tail_tiles ? 1000 / s.tail_splits + 270 : 0);
+        };
+        const Step head = make_plan(T - rest, D, F, asked).gate_up;
+        const int64_t rest_milli = 900 * (int64_t)p.gate_up.tiles_m / kBlockTarget;
+        if (head.kind == K_GEMM_GU_L && rounds_milli(head) + rest_milli < rounds_milli(p.gate_up)) {
+            p.gate_up = head;
+            p.gate_up_rest = make_plan(rest, D, F, asked).gate_up;
+            p.rest_row = T - rest;
+        }
+    }
     return p;
 }
 
@@ -525,8 +559,8 @@ Layout make_layout(int64_t T, int64_t D, int64_t F)
         if (path == GMLP_PATH_GEMV && T > kGemvMaxTokens)
             continue;
         const Plan p = make_plan(T, D, F, path);
-        counters = std::max({counters, p.gate_up.counters, p.down.counters});
-        partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes});
+        counters = std::max({counters, p.gate_up.counters, p.down.counters, p.gate_up_rest.counters});
+        partial = std::max({partial, p.gate_up.partial_bytes, p.down.partial_bytes, p.gate_up_rest.partial_bytes});
         if (path == GMLP_PATH_GEMV) // the fused kernel runs both steps at once: separate partial sums
             partial = std::max(partial, align_up(p.gate_up.partial_bytes) + p.down.partial_bytes);
     }

@@ -63,7 +63,8 @@ int main()
 {
     const std::vector<int64_t> Ts = {1, 2, 3, 5, 6, 7, 8, 9, 15, 16, 17, 31, 32, 33, 48, 63, 64, 65,
                                      80, 96, 97, 100, 127, 128, 129, 200, 255, 256, 257, 300, 384, 511, 512, 640,
-                                     768, 1000, 1024, 1280, 1536, 2048, 4096, 4352, 37601, 1 << 20, 1 << 24};
+                                     520, 600, 768, 1000, 1024, 1088, 1280, 1536, 1600, 2048, 4096, 4352, 37601,
+                                     1 << 20, 1 << 24};
     const std::vector<int64_t> dims = {8, 72, 136, 256, 264, 520, 1032, 2056, 4096, 4104, 4352, 8192,
                                        14336, 14464, 28672, 1 << 16, 1 << 22};
     int plans = 0;
@@ -84,6 +85,13 @@ int main()
                     const Plan p = make_plan(T, D, F, path);
                     check_step(p.gate_up, l, T, D, F);
                     check_step(p.down, l, T, D, F);
+                    if (p.rest_row) { // a token split of the gate/up step
+                        check_step(p.gate_up_rest, l, T, D, F);
+                        EXPECT(p.rest_row > 0 && p.rest_row < T && p.gate_up.N == p.rest_row &&
+                                   p.gate_up_rest.N == T - p.rest_row && p.gate_up.M == F && p.gate_up_rest.M == F,
+                               "token split of T=%lld at %lld", (long long)T, (long long)p.rest_row);
+                    } else
+                        EXPECT(p.gate_up.N == T, "gate/up rows");
                     if (p.path == GMLP_PATH_FUSED || p.path == GMLP_PATH_FUSED_MFMA)
                         EXPECT(fused_grid(p) == p.gate_up.blocks + p.down.blocks, "fused grid");
                     if (p.path == GMLP_PATH_FUSED_MFMA) {

@@ -208,6 +208,31 @@ def test_192_token_tiles(orc, T, D, F):
     _check(gmlp.to_bf16_bits(y)[rows], Y_ref, "192-token Y T=%d D=%d F=%d" % (T, D, F))
 
 
+# From 513 tokens the gate/up step may run on a token split: the whole
+# 256-token tiles of the first T - r rows, then the last r rows as a
+# problem of their own (GEMV kernels for r <= 5, few-token tiles, pairs).
+TOKEN_SPLIT = [(515, 1032, 14344), (520, 264, 14344), (600, 1032, 14344), (1100, 520, 14344)]
+
+
+@pytest.mark.parametrize("T,D,F", TOKEN_SPLIT, ids=["T%dD%dF%d" % s for s in TOKEN_SPLIT])
+def test_gate_up_token_split(orc, T, D, F):
+    r = T % 256
+    plan = gmlp.describe(T, D, F)
+    assert plan[0][0] == "gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4, 2, 64>, 0, false, false>", plan
+    assert plan[1][0].startswith("gemv_splitk_kernel<%d, 2," % r) if r <= 5 else plan[1][3] == 2, plan
+    X, Wg, Wu, Wd = I.generate(T, D, F, seed=T + D + F)
+    x, wg, wu, wd = (_dev(a) for a in (X, Wg, Wu, Wd))
+    ws = gmlp.Workspace(T, D, F)
+    edge = np.arange(T - r - 3, T - r + 3)
+    rows = np.unique(np.concatenate([I.sample_rows(T, 16), edge, np.arange(T - 3, T)]))
+    h = gmlp.gate_up(x, wg, wu, workspace=ws)
+    y = gmlp.forward(x, wg, wu, wd, workspace=ws)
+    torch.cuda.synchronize()
+    Y_ref, H_ref = orc.gated_mlp_rows(X, Wg, Wu, Wd, rows=rows, return_h=True)
+    _check(gmlp.to_bf16_bits(h)[rows], H_ref, "token-split H T=%d D=%d F=%d" % (T, D, F))
+    _check(gmlp.to_bf16_bits(y)[rows], Y_ref, "token-split Y T=%d D=%d F=%d" % (T, D, F))
+
+
 # Each GEMV strip's arrival counter sits on a 128-byte line of its own
 # where both steps' counters fit the counter block so (up to 512 strips in
 # all); past that, on consecutive words.  514 strips (F = 262152): the
@@ -339,11 +364,11 @@ def test_few_token_tiles_at_model_dims(orc, T):
     _run(T, 4096, 14336, seed=60 + T, rows=I.sample_rows(T, 8), orc=orc)
 
 
-@pytest.mark.parametrize("T,D,F", [(640, 264, 14336), (4096, 4352, 2056)])
+@pytest.mark.parametrize("T,D,F", [(704, 264, 14336), (4096, 4352, 2056)])
 def test_tail_tiles_split_over_k(orc, T, D, F):
     # 256-token tiles that leave a last round of blocks at most half full:
     # the whole rounds run as one launch, the remaining tiles as a second,
-    # split-K launch (T = 640: 336 gate/up tiles = 256 + 80 split 3 ways;
+    # split-K launch (T = 704: 336 gate/up tiles = 256 + 80 split 2 ways;
     # the second shape has tails in both steps, 272 tiles each).
     plan = gmlp.describe(T, D, F)
     assert any(", true, false>" in k and "GemmShape<2, 4, 2, 1, 4" in k for k, *_ in plan)

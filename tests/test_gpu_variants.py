@@ -63,6 +63,16 @@ def test_variant_paired_gate_up_blocks(orc, name, T):
 
 
 @pytest.mark.parametrize("name", sorted(VARIANTS))
+@pytest.mark.parametrize("T", [515, 600])
+def test_variant_gate_up_token_split(orc, name, T):
+    # The gate/up step on a token split (the rest rows through the GEMV
+    # kernels at T = 515, through pairs at T = 600), RMSNorm scales included.
+    assert len(gmlp.describe(T, 1032, 14344)) == 3
+    rows = np.unique(np.concatenate([I.sample_rows(T, 12), np.arange(509, 515)]))
+    _run(orc, T, 1032, 14344, VARIANTS[name], seed=50 + T, rows=rows, x_scale=3.0)
+
+
+@pytest.mark.parametrize("name", sorted(VARIANTS))
 @pytest.mark.parametrize("T", [2, 5])
 def test_variant_on_the_mfma_path_at_small_T(orc, name, T):
     _run(orc, T, 520, 1032, VARIANTS[name], seed=90 + T, path="mfma", x_scale=0.25)

@@ -49,55 +49,98 @@ def _steps(plan):
     return steps
 
 
+def _check_step(step, lines, M, K, T):
+    """One step's launches cover its M x T outputs over K."""
+    for name, grid, block, splits in lines:
+        assert grid >= 1 and splits >= 1 and block in (256, 512)
+    name, grid, block, splits = lines[0]
+    if name.startswith("gemv"):
+        # The automatic path takes the GEMV kernels up to 5 tokens.
+        assert len(lines) == 1
+        assert T <= 5 and name.startswith("gemv_splitk_kernel<%d," % T)
+        # Up to 2 tokens: 8-wave blocks; the gate/up step reads 1 KB row
+        # segments (512-column strips), the down step 512 bytes (256).
+        # Above, 4-wave blocks of 256-column strips.
+        assert block == (512 if T <= 2 else 256)
+        strips = _cdiv(M, 512 if T <= 2 and step == 0 else 256)
+        assert grid == strips * splits
+        assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
+        return
+    assert T > 5
+    bmw, bn = _tile(name)
+    tiles = _cdiv(M, bmw) * _cdiv(T, bn)
+    # Every tile is computed by exactly one launch of the step.
+    assert sum(g // sp for _, g, _, sp in lines) == tiles
+    for name_i, grid_i, _, splits_i in lines:
+        assert _tile(name_i) == (bmw, bn) and grid_i % splits_i == 0
+        _, split_k, streamed = _flags(name_i)
+        # Weights take the streaming cache policy exactly when one token
+        # tile reads each of them once.
+        assert streamed == (_cdiv(T, bn) == 1)
+        if splits_i > 1:
+            assert split_k
+            assert splits_i * 4 * bmw * bn * 2 * (grid_i // splits_i) <= 2 ** 31  # partials addressable
+        if _flags(name_i)[0] == 2:
+            # A G and a U block per column tile of one token tile, where
+            # the dual-B plan would split K in two or run two 128-token
+            # tiles: 65 to 192 tokens.
+            assert step == 0 and splits_i == 2 and 65 <= T <= 192 and _cdiv(T, bn) == 1
+            assert 96 < grid_i // 2 <= 128  # two-way split of more than 3/4 of a round
+    if len(lines) == 2:
+        # Tail launch: whole rounds of 256 blocks first, then a partial
+        # round of at most half the chip split over K.
+        (_, g0, _, s0), (_, g1, _, s1) = lines
+        assert s0 == 1 and g0 % 256 == 0 and 0 < g1 // s1 <= 128 and 2 <= s1 <= 8 and g1 <= 256
+    else:
+        assert len(lines) == 1
+
+
+def _gate_up_lines(T, D, F):
+    return _steps(gmlp.describe(T, D, F))[0][1]
+
+
+SPLITS = [(T, 4096, 14336, split) for T, split in [(512, False), (513, True), (520, True), (640, True), (704, False),
+                                                   (768, False), (1088, True), (1600, True), (1800, False), (2048, False),
+                                                   (2112, False), (2340, True), (2880, True)]]
+SPLITS += [(T, 8192, 28672, split) for T, split in [(800, False), (1100, True), (1600, True), (2048, False)]]
+
+
+@pytest.mark.parametrize("T,D,F,split", SPLITS)
+def test_gate_up_token_split(T, D, F, split):
+    """The gate/up step runs on a token split where the last token tile of
+    the 256-token tiles holds at most 128 tokens and the fitted round cost
+    of the split plan is lower (the cases measured); the down step keeps
+    one plan over all T rows."""
+    (_, gu), (_, dn) = _steps(gmlp.describe(T, D, F))
+    r = T % 256
+    if split:
+        assert gu == _gate_up_lines(T - r, D, F) + _gate_up_lines(r, D, F)
+    else:
+        assert gu[0][0].startswith("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4, 2, 64>")
+        assert all(_tile(line[0]) == (128, 256) for line in gu)
+    assert dn == _steps(gmlp.describe(T, D, F))[1][1]
+
+
 @settings(max_examples=300, deadline=None)
 @given(T=tokens, D=dims, F=dims)
 def test_gated_mlp_plan_covers_the_problem(T, D, F):
     plan = gmlp.describe(T, D, F)
     steps = _steps(plan)
     assert [s for s, _ in steps] == [0, 1]
-    for (step, lines), (M, K) in zip(steps, [(F, D), (D, F)]):
-        for name, grid, block, splits in lines:
-            assert grid >= 1 and splits >= 1 and block in (256, 512)
-        name, grid, block, splits = lines[0]
-        if name.startswith("gemv"):
-            # The automatic path takes the GEMV kernels up to 5 tokens.
-            assert len(lines) == 1
-            assert T <= 5 and name.startswith("gemv_splitk_kernel<%d," % T)
-            # Up to 2 tokens: 8-wave blocks; the gate/up step reads 1 KB row
-            # segments (512-column strips), the down step 512 bytes (256).
-            # Above, 4-wave blocks of 256-column strips.
-            assert block == (512 if T <= 2 else 256)
-            strips = _cdiv(M, 512 if T <= 2 and step == 0 else 256)
-            assert grid == strips * splits
-            assert splits <= _cdiv(K, 16)  # each split holds at least one 16-row batch
-            continue
-        assert T > 5
-        bmw, bn = _tile(name)
-        tiles = _cdiv(M, bmw) * _cdiv(T, bn)
-        # Every tile is computed by exactly one launch of the step.
-        assert sum(g // sp for _, g, _, sp in lines) == tiles
-        for name_i, grid_i, _, splits_i in lines:
-            assert _tile(name_i) == (bmw, bn) and grid_i % splits_i == 0
-            _, split_k, streamed = _flags(name_i)
-            # Weights take the streaming cache policy exactly when one token
-            # tile reads each of them once.
-            assert streamed == (_cdiv(T, bn) == 1)
-            if splits_i > 1:
-                assert split_k
-                assert splits_i * 4 * bmw * bn * 2 * (grid_i // splits_i) <= 2 ** 31  # partials addressable
-            if _flags(name_i)[0] == 2:
-                # A G and a U block per column tile of one token tile, where
-                # the dual-B plan would split K in two or run two 128-token
-                # tiles: 65 to 192 tokens.
-                assert step == 0 and splits_i == 2 and 65 <= T <= 192 and _cdiv(T, bn) == 1
-                assert 96 < grid_i // 2 <= 128  # two-way split of more than 3/4 of a round
-        if len(lines) == 2:
-            # Tail launch: whole rounds of 256 blocks first, then a partial
-            # round of at most half the chip split over K.
-            (_, g0, _, s0), (_, g1, _, s1) = lines
-            assert s0 == 1 and g0 % 256 == 0 and 0 < g1 // s1 <= 128 and 2 <= s1 <= 8 and g1 <= 256
-        else:
-            assert len(lines) == 1
+    (_, gu), (_, dn) = steps
+    # A token split of the gate/up step: the whole 256-token tiles of the
+    # first T - r rows, then the last r <= 128 rows planned on their own,
+    # from 513 tokens.
+    r = T % 256
+    split = 0 < r <= 128 and T > 512 and gu == _gate_up_lines(T - r, D, F) + _gate_up_lines(r, D, F)
+    if split:
+        head = _gate_up_lines(T - r, D, F)
+        assert head[0][0].startswith("gemm_mfma_kernel<GemmShape<2, 4, 2, 1, 4, 2, 64>")
+        _check_step(0, head, F, D, T - r)
+        _check_step(0, gu[len(head):], F, D, r)
+    else:
+        _check_step(0, gu, F, D, T)
+    _check_step(1, dn, D, F, T)
     ws = gmlp.workspace_size(T, D, F)
     assert ws >= T * F * 2  # holds H
     assert ws % 256 == 0
