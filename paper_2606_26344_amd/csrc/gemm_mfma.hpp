@@ -665,7 +665,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             // it stored) and stores that pass's outputs before the next.
             // Keeping the accumulators live through the reduction and the
             // epilogue spilled registers.
-            constexpr int CH = 8;
+            constexpr int CH = PIECES % 8 == 0 ? 8 : 4;
             static_assert(PIECES % CH == 0, "whole passes");
             const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.out + (size_t)n0 * M + m0);
 #pragma unroll
@@ -703,11 +703,11 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
             return m0;
         }
         // Pieces are summed CH at a time: all of them for up to 16; the
-        // 256 x 256 tiles take four passes of 8, which keeps the loaded
-        // pieces and the sums within the register budget next to the
-        // accumulators.  Piece g = ((w * TM + mi) * TN + ni) * 4 + j holds
+        // 256 x 256 tiles take four passes of 8 (tiles of 20 pieces five
+        // of 4), which keeps the loaded pieces and the sums within the
+        // register budget next to the accumulators.  Piece g = ((w * TM + mi) * TN + ni) * 4 + j holds
         // accumulators 4j .. 4j+3 of acc[w][mi][ni].
-        constexpr int CH = PIECES > 16 ? 8 : PIECES;
+        constexpr int CH = PIECES <= 16 ? PIECES : PIECES % 8 == 0 ? 8 : 4;
         static_assert(PIECES % CH == 0, "whole passes");
         auto get_piece = [&](int g) __attribute__((always_inline)) {
             return acc[g / (4 * TN * TM)][g / (4 * TN) % TM][g / 4 % TN].piece(g % 4);

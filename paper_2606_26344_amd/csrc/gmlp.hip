@@ -197,6 +197,8 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
             return launch_gemm<PairMid96, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
         if (s.N <= PairSmall::BN)
             return launch_gemm<PairSmall, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        if (s.N <= PairMid160::BN)
+            return launch_gemm<PairMid160, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
         return launch_gemm<PairMid192, EPI_GATE_PAIR, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
     case K_GEMV:
         return v.rms ? launch_gemv<2, EPI_GATE_MUL, true>(s, Wg, Wu, X, H, ws, l, v, st)

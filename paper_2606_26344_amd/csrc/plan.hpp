@@ -79,6 +79,7 @@ using FusedDownMid = GemmShape<1, 4, 1, 1, 2, 4, 64>;
 // a 192-token tile.
 using PairMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>; // 128 F cols x 96 tokens, 4 waves
 using PairSmall = GemmShape<1, 2, 2, 2, 2, 3, 64>; // 128 F cols x 128 tokens, 4 waves
+using PairMid160 = GemmShape<1, 4, 1, 1, 5, 3, 64>; // 128 F cols x 160 tokens, 4 waves
 using PairMid192 = GemmShape<1, 4, 1, 1, 6, 3, 64>; // 128 F cols x 192 tokens, 4 waves
 // 257 to 384 tokens: two 192-token tiles (a quarter less work and
 // activation staging than two 256-token tiles at T = 384, a quarter more at
@@ -443,10 +444,16 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     // instead of twice per column tile.  Measured at D = 4096, F = 14336,
     // gate/up alone: T = 129 68.5 -> 67.4 us, 160 70.9 -> 68.4, 192 74.3 ->
     // 68.6-68.8; pairs of 256-token tiles for T = 193..256 were slower (T =
-    // 224: 77.7 -> 89-91 us).
+    // 224: 77.7 -> 89-91 us).  Up to 160 tokens a 160-token tile stages a
+    // sixth less X and does a sixth less MFMA work: T = 129 67.9 -> 58.3
+    // us, 144 69.4 -> 58.6, 160 69.0 -> 59.3.
     if (p.gate_up.kind == K_GEMM_GU_S && p.gate_up.tiles_n == 2 && p.gate_up.splits == 1 && T <= PairMid192::BN &&
-        p.gate_up.blocks >= kPairMinBlocks && p.gate_up.blocks <= kBlockTarget)
-        pair_step<PairMid192>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
+        p.gate_up.blocks >= kPairMinBlocks && p.gate_up.blocks <= kBlockTarget) {
+        if (T <= PairMid160::BN)
+            pair_step<PairMid160>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
+        else
+            pair_step<PairMid192>(p.gate_up, (int)F, (int)T, (int)D, kGroupGateUp);
+    }
     // Down: large tiles once there are enough of them to fill the chip.
     // Above one token tile, from 40 of them up to a round, large tiles split over K to fill one
     // round beat two rounds of 128 x 128 tiles (measured: D = 4096, F = 14336
@@ -730,6 +737,7 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_GU_P: {
         const std::string shape = s.N <= PairMid96::BN   ? shape_name<PairMid96>()
                                   : s.N <= PairSmall::BN ? shape_name<PairSmall>()
+                                  : s.N <= PairMid160::BN ? shape_name<PairMid160>()
                                                          : shape_name<PairMid192>();
         return "gemm_mfma_kernel<" + shape + ", 2, true, true>";
     }
