@@ -250,6 +250,8 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
                                                                                 nullptr, rowdiv, st);
     case K_GEMM_DN_X:
         return launch_gemm<DownWide, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
+    case K_GEMM_DN_Q: // one token tile: always streamed
+        return launch_gemm<DownMid160, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
     case K_GEMM_DN_Y:
         return stream_weights(s) ? launch_gemm<DownMid192, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,
                                                                                   nullptr, rowdiv, st)

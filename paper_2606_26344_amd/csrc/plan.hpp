@@ -67,6 +67,7 @@ using DownMid = GemmShape<1, 4, 1, 1, 2, 6, 64>;    // 128 D cols x 64 tokens, 4
 // 64 tokens the 64-token tiles stay 8% faster).
 using GateUpMid96 = GemmShape<2, 4, 1, 1, 3, 3, 64>; // 128 F cols x 96 tokens, 4 waves
 using DownMid96 = GemmShape<1, 4, 1, 1, 3, 5, 64>;   // 128 D cols x 96 tokens, 4 waves
+using DownMid160 = GemmShape<1, 4, 1, 1, 5, 3, 64>;  // 128 D cols x 160 tokens, 4 waves
 using DownMid192 = GemmShape<1, 4, 1, 1, 6, 3, 64>;  // 128 D cols x 192 tokens, 4 waves
 // The down steps of the one-launch MFMA kernel: the same tiles with 4 LDS
 // stages, so that one LDS array per stage, shared with the gate/up step's,
@@ -137,7 +138,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 enum Kind {
     K_NONE,
     K_GEMM_GU_L, K_GEMM_GU_S, K_GEMM_GU_W, K_GEMM_GU_M, K_GEMM_GU_T, K_GEMM_GU_P, K_GEMM_GU_Y,
-    K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMM_DN_X, K_GEMM_DN_Y,
+    K_GEMM_DN_L, K_GEMM_DN_S, K_GEMM_DN_W, K_GEMM_DN_M, K_GEMM_DN_T, K_GEMM_DN_X, K_GEMM_DN_Y, K_GEMM_DN_Q,
     K_GEMV
 };
 
@@ -495,6 +496,11 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     // 128-token tiles, so each weight element is read once (measured:
     // steps at D = 4096, F = 14336 T = 129 109.6 -> 108.8 us, 160 112.1 ->
     // 110.1, 192 115.4 -> 111.2; D = 8192, F = 28672 T = 160 454.8 -> 412.9).
+    // Up to 160 tokens a 160-token tile (down at D = 8192, F = 28672: T =
+    // 129 108.2-109.6 -> 98.0-98.5 us, 150 111.4 -> 100.4; equal at
+    // D = 4096, F = 14336).
+    else if (T > DownSmall::BN && T <= DownMid160::BN)
+        gemm_step<DownMid160>(p.down, K_GEMM_DN_Q, (int)D, (int)T, (int)F, 1, true, kGroupDown);
     else if (T > DownSmall::BN && T <= DownMid192::BN)
         gemm_step<DownMid192>(p.down, K_GEMM_DN_Y, (int)D, (int)T, (int)F, 1, true, kGroupDown);
     else
@@ -732,6 +738,7 @@ std::string kernel_name(const Step &s, bool gate_up)
     case K_GEMM_GU_W: return "gemm_mfma_kernel<" + shape_name<GateUpMid96>() + ", 0, true, true>";
     case K_GEMM_GU_Y: return "gemm_mfma_kernel<" + shape_name<GateUp192>() + ", 0, false, false>";
     case K_GEMM_DN_W: return "gemm_mfma_kernel<" + shape_name<DownMid96>() + ", 1, true, true>";
+    case K_GEMM_DN_Q: return "gemm_mfma_kernel<" + shape_name<DownMid160>() + ", 1, true, true>";
     case K_GEMM_DN_Y:
         return "gemm_mfma_kernel<" + shape_name<DownMid192>() + ", 1, true, " + (stream_weights(s) ? "true>" : "false>");
     case K_GEMM_GU_P: {

@@ -184,6 +184,14 @@ def test_paired_gate_up_blocks(orc, T, D, F):
     _check(gmlp.to_bf16_bits(y)[rows], Y_ref, "paired Y T=%d D=%d F=%d" % (T, D, F))
 
 
+@pytest.mark.parametrize("T,D,F", [(150, 8200, 4104), (137, 2056, 3080)])
+def test_160_token_down_tiles(orc, T, D, F):
+    # 129 to 160 tokens: one 160-token down tile split over K (ragged D and
+    # F, 3 and 13 splits).
+    assert gmlp.describe(T, D, F)[-1][0] == "gemm_mfma_kernel<GemmShape<1, 4, 1, 1, 5, 3, 64>, 1, true, true>"
+    _run(T, D, F, seed=T + D, rows=np.unique(np.concatenate([I.sample_rows(T, 16), np.arange(T - 4, T)])), orc=orc)
+
+
 # 257 to 384 tokens: two 192-token tiles in both steps (the gate/up step
 # where they fill 3/4 of a round to one round, the down step where it has
 # 64 to 128 tiles), with a ragged second token tile and ragged D and F.
