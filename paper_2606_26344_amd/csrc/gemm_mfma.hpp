@@ -73,8 +73,13 @@ struct GemmParams {
     int group_m; // consecutive blocks sweep group_m column tiles before the next token tile
     // This launch computes tiles [tile_base, tile_base + tile_count) of the
     // block order of all tiles_m x tiles_n tiles (a plan can give the tiles
-    // of a last, partial round of blocks to a split-K launch of their own).
+    // of a last, partial round of blocks to a split-K part of their own).
     int tile_base, tile_count;
+    // A split-K launch may start with head_blocks blocks (a multiple of 8)
+    // that each compute one whole tile over all of K: tiles [0, head_blocks)
+    // of the block order, before its split tiles, so those start as soon as
+    // CUs free up instead of after the last whole tile.
+    int head_blocks;
     // Gate/up epilogue: activation (enum Activation), swish slope, and the
     // per-token RMSNorm scales [N] (nullptr: none).
     int activation;
@@ -213,12 +218,15 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % S::WM, wn = wave / S::WM;
 
-    // Block -> (split, tile), as gemm_split_of_block.
-    const int ntiles = p.tile_count; // tiles of this launch
-    const int id = xcd_contiguous_id(block, ntiles * p.splits);
-    const int split = id / ntiles;
-    const int local = id - split * ntiles; // tile within the launch: split-K counter and partial slot
-    const int tile_id = p.tile_base + local;
+    // Block -> (split, tile), as gemm_split_of_block; the head blocks of a
+    // split-K launch take whole tiles (split 0 of 1).
+    const bool head = SPLIT && block < p.head_blocks;
+    const int ntiles = p.tile_count; // split tiles of this launch
+    const int id = head ? xcd_contiguous_id(block, p.head_blocks)
+                        : xcd_contiguous_id(block - (SPLIT ? p.head_blocks : 0), ntiles * p.splits);
+    const int split = head ? 0 : id / ntiles;
+    const int local = head ? id : id - split * ntiles; // split tiles: counter and partial slot
+    const int tile_id = head ? id : p.tile_base + local;
     const int per_group = p.group_m * p.tiles_n;
     const int group = tile_id / per_group;
     const int first_m = group * p.group_m;
@@ -233,7 +241,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     constexpr bool PAIR = EPI == EPI_GATE_PAIR;
     static_assert(!PAIR || (NW == 1 && SPLIT), "a pair is two blocks of one weight each");
     const int kb = PAIR ? 0 : split * p.k_split;
-    const int ke = PAIR ? K : min(K, kb + p.k_split);
+    const int ke = PAIR || head ? K : min(K, kb + p.k_split);
     const uint16_t *w_first = PAIR && split ? p.w1 : p.w0;
     const int nk = (ke - kb + S::BK - 1) / S::BK;
     const bool ragged_k = (ke - kb) % S::BK != 0; // last k-tile is partial
@@ -578,7 +586,7 @@ __device__ __forceinline__ int gemm_block(const GemmParams &p, int block, StageP
     // pieces with device-coherent loads (up to 16 pieces of a split in flight
     // at once) and adds the splits in order 0, 1, 2, ...  No cache-wide
     // write-back or invalidate is needed.
-    if (SPLIT && p.splits > 1) {
+    if (SPLIT && p.splits > 1 && !head) {
         constexpr int PIECES = NW * TM * TN * 4; // 4 accumulators (16 bytes) per piece
         const __amdgpu_buffer_rsrc_t prs = make_rsrc(p.partial);
         const uint32_t lane_off = lane * 16;

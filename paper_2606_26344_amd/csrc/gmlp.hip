@@ -66,6 +66,7 @@ GemmParams gemm_params(const Step &s, const void *w0, const void *w1, const void
     p.group_m = s.group_m;
     p.tile_base = s.tile_base;
     p.tile_count = s.tile_count;
+    p.head_blocks = 0;
     p.activation = v.act;
     p.beta = v.beta;
     p.rrms = rrms;
@@ -76,15 +77,19 @@ GemmParams gemm_params(const Step &s, const void *w0, const void *w1, const void
 template <class S, int EPI, bool SPLIT, bool STREAM_W = false>
 int launch_gemm(const Step &s, const void *w0, const void *w1, const void *act, void *out,
                 uint8_t *ws, const Layout &l, const Variant &v, const float *rrms, const float *rowdiv,
-                hipStream_t stream)
+                hipStream_t stream, int head_blocks = 0)
 {
-    const GemmParams p = gemm_params(s, w0, w1, act, out, ws, l, v, rrms, rowdiv);
+    GemmParams p = gemm_params(s, w0, w1, act, out, ws, l, v, rrms, rowdiv);
+    if (head_blocks && (!SPLIT || head_blocks % 8 != 0))
+        return fail(GMLP_ERR_INVALID_ARG, "internal: %d whole-tile head blocks", head_blocks);
+    p.head_blocks = head_blocks;
     if (!SPLIT && s.splits != 1)
         return fail(GMLP_ERR_INVALID_ARG, "internal: split-K plan for a kernel without split-K");
     if (s.partial_bytes > (size_t)kNumRecords)
         return fail(GMLP_ERR_UNSUPPORTED, "split-K partial sums of %zu bytes exceed the 2 GiB buffer range",
                     s.partial_bytes);
-    hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT, STREAM_W>), dim3(s.blocks), dim3(S::NTHREADS), 0, stream, p);
+    hipLaunchKernelGGL((gemm_mfma_kernel<S, EPI, SPLIT, STREAM_W>), dim3(head_blocks + s.blocks), dim3(S::NTHREADS), 0,
+                       stream, p);
     return hip_check(hipGetLastError(), "MFMA GEMM launch");
 }
 
@@ -172,10 +177,10 @@ int run_gate_up(const Step &s, const void *X, const void *Wg, const void *Wu, vo
     }
     switch (s.kind) {
     case K_GEMM_GU_L: {
-        const int rc = launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
-        if (rc || !s.tail_tiles)
-            return rc;
-        return launch_gemm<GateUpLarge, EPI_GATE_MUL, true>(tail_step(s), Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        if (!s.tail_tiles)
+            return launch_gemm<GateUpLarge, EPI_GATE_MUL, false>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st);
+        return launch_gemm<GateUpLarge, EPI_GATE_MUL, true>(tail_step(s), Wg, Wu, X, H, ws, l, v, rrms, nullptr, st,
+                                                            s.tile_count);
     }
     case K_GEMM_GU_S:
         return stream_weights(s) ? launch_gemm<GateUpSmall, EPI_GATE_MUL, true, true>(s, Wg, Wu, X, H, ws, l, v, rrms, nullptr, st)
@@ -229,12 +234,10 @@ int run_down(const Step &s, const void *H, const void *Wd, void *Y, uint8_t *ws,
     case K_GEMM_DN_L: {
         if (s.splits > 1)
             return launch_gemm<DownLarge, EPI_STORE, true>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
-        const int rc = launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv,
-                                                                 st);
-        if (rc || !s.tail_tiles)
-            return rc;
+        if (!s.tail_tiles)
+            return launch_gemm<DownLarge, EPI_STORE, false>(s, Wd, nullptr, H, Y, ws, l, plain, nullptr, rowdiv, st);
         return launch_gemm<DownLarge, EPI_STORE, true>(tail_step(s), Wd, nullptr, H, Y, ws, l, plain, nullptr,
-                                                        rowdiv, st);
+                                                        rowdiv, st, s.tile_count);
     }
     case K_GEMM_DN_S:
         return stream_weights(s) ? launch_gemm<DownSmall, EPI_STORE, true, true>(s, Wd, nullptr, H, Y, ws, l, plain,

@@ -156,17 +156,17 @@ struct Step {
     size_t partial_bytes = 0; // fp32 split-K partial sums
     int counters = 0;         // arrival counters
     // GEMM without split-K whose tiles leave a last round of blocks at most
-    // half full: the first tile_count tiles (whole rounds) run as planned,
-    // the last tail_tiles run in a second launch split tail_splits ways over
-    // K (tail_k_split rows each), so they fill a round instead of idling most
-    // of the chip.
+    // half full: the first tile_count tiles (whole rounds) take one block
+    // each, the last tail_tiles tail_splits blocks each over K (tail_k_split
+    // rows each), so they fill a round instead of idling most of the chip;
+    // both run as one split-K launch, the whole tiles' blocks first.
     int tile_base = 0, tile_count = 0;
     int tail_tiles = 0, tail_splits = 1, tail_k_split = 0;
     int64_t block_macs = 0; // GEMM: multiply-adds of one block of the main launch
 };
 
-// The second launch of a step with a tail: its last tail_tiles tiles, split
-// over K.
+// The split part of a step with a tail: its last tail_tiles tiles, split
+// over K (launched after the step's tile_count whole-tile blocks).
 Step tail_step(const Step &s)
 {
     Step t = s;
@@ -267,7 +267,7 @@ void gemm_step(Step &s, Kind kind, int M, int N, int K, int nw, bool allow_split
     s.threads = S::NTHREADS;
     s.counters = std::max(s.splits > 1 ? tiles : 0, s.tail_tiles);
     // Partial sums of whole tiles (padded), [split][tile][wave][piece][lane];
-    // the tail launch runs after the main one and reuses the space.
+    // the tail tiles use the space of a split step's partial sums.
     const size_t tile_bytes = (size_t)S::BMW * S::BN * nw * sizeof(float);
     s.partial_bytes = std::max(s.splits > 1 ? (size_t)s.splits * tiles * tile_bytes : 0,
                                (size_t)s.tail_splits * s.tail_tiles * tile_bytes);
@@ -526,7 +526,7 @@ Plan make_plan(int64_t T, int64_t D, int64_t F, int path)
     // whole 256-token tiles (few-token tiles that stream the weights,
     // mostly from the last-level cache) instead of padding them to 256
     // tokens.  The choice follows a cost in rounds of full-K tiles fitted
-    // to measurements: a partial round costs a round, a tail launch split s
+    // to measurements: a partial round costs a round, tail tiles split s
     // ways 1/s + 0.27, the r-token problem 0.9 C / 256 for C column tiles
     // (it streams weights that a round of tiles reads in about 280 tiles'
     // time).  Gate/up at D = 4096, F = 14336: T = 520 176.0 -> 148.9 us,
@@ -764,21 +764,22 @@ std::string fused_kernel_name(const Plan &plan)
     return "gemm_fused_kernel<" + shape_name<GateUpMid>() + ", " + shape_name<FusedDownMid>() + ">";
 }
 
-// The describe lines of a step: its launch, then its tail launch if any.
+// The describe line of a step's launch.
 std::string describe_step(const Step &s, bool gate_up)
 {
     char tmp[200];
-    snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", kernel_name(s, gate_up).c_str(), s.blocks,
-             s.threads, s.splits);
-    std::string text = tmp;
     if (s.tail_tiles) {
+        // One split-K launch: the whole tiles first, one block each over
+        // all of K, then the tail tiles' splits.
         const Step t = tail_step(s);
         const std::string shape = s.kind == K_GEMM_GU_L ? shape_name<GateUpLarge>() + ", 0" : shape_name<DownLarge>() + ", 1";
         snprintf(tmp, sizeof tmp, "gemm_mfma_kernel<%s, true, false> grid=%d block=%d k_splits=%d\n", shape.c_str(),
-                 t.blocks, t.threads, t.splits);
-        text += tmp;
+                 s.tile_count + t.blocks, t.threads, t.splits);
+        return tmp;
     }
-    return text;
+    snprintf(tmp, sizeof tmp, "%s grid=%d block=%d k_splits=%d\n", kernel_name(s, gate_up).c_str(), s.blocks,
+             s.threads, s.splits);
+    return tmp;
 }
 
 int check_gate_up_args(const void *X, const void *Wg, const void *Wu, const void *H, int64_t T,

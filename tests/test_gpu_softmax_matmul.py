@@ -109,9 +109,11 @@ def test_benchmark_shape_sampled_rows(sorc):
 
 
 def test_matmul_tail_tiles_split_over_k(sorc):
-    # 16 x 17 = 272 tiles of 256 x 256: one round, then 16 tiles split over K.
+    # 16 x 17 = 272 tiles of 256 x 256: one round of whole tiles, then, in
+    # the same launch, 16 tiles split over K.
     M, K, N = 4096, 2056, 4352
-    assert len(smm.describe(M, K, N)) == 3
+    plan = smm.describe(M, K, N)
+    assert len(plan) == 2 and plan[1][3] > 1 and plan[1][1] == 256 + 16 * plan[1][3], plan
     _run(sorc, M, K, N, seed=41, rows=I.sample_rows(M, 32))
 
 

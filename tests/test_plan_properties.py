@@ -69,8 +69,18 @@ def _check_step(step, lines, M, K, T):
     assert T > 5
     bmw, bn = _tile(name)
     tiles = _cdiv(M, bmw) * _cdiv(T, bn)
-    # Every tile is computed by exactly one launch of the step.
-    assert sum(g // sp for _, g, _, sp in lines) == tiles
+    assert len(lines) == 1
+    if splits > 1 and grid != tiles * splits:
+        # A tail: whole rounds of 256 tiles, one block each over all of K,
+        # then, in the same launch, a partial round of at most half the chip
+        # split 2 to 8 ways over K.
+        assert _tile(name) in ((128, 256), (256, 256)) and _flags(name)[1]
+        whole, tail = tiles // 256 * 256, tiles % 256
+        assert whole >= 256 and 0 < tail <= 128 and 2 <= splits <= 8
+        assert grid == whole + tail * splits and tail * splits <= 256
+        return
+    # Every tile is computed by exactly one block, or by one block per split.
+    assert grid == tiles * splits
     for name_i, grid_i, _, splits_i in lines:
         assert _tile(name_i) == (bmw, bn) and grid_i % splits_i == 0
         _, split_k, streamed = _flags(name_i)
@@ -86,13 +96,6 @@ def _check_step(step, lines, M, K, T):
             # tiles: 65 to 192 tokens.
             assert step == 0 and splits_i == 2 and 65 <= T <= 192 and _cdiv(T, bn) == 1
             assert 96 < grid_i // 2 <= 128  # two-way split of more than 3/4 of a round
-    if len(lines) == 2:
-        # Tail launch: whole rounds of 256 blocks first, then a partial
-        # round of at most half the chip split over K.
-        (_, g0, _, s0), (_, g1, _, s1) = lines
-        assert s0 == 1 and g0 % 256 == 0 and 0 < g1 // s1 <= 128 and 2 <= s1 <= 8 and g1 <= 256
-    else:
-        assert len(lines) == 1
 
 
 def _gate_up_lines(T, D, F):
@@ -188,9 +191,8 @@ def test_softmax_matmul_plan(M, K, N):
     assert r == 16 or 512 * r >= K  # the row fits in registers unless streamed
     mm = plan[1:]
     if mm[0][0].startswith("gemm"):
-        # The matmul's launches (a tail launch included) cover its tiles once.
-        bmw, bn = _tile(mm[0][0])
-        assert sum(g // sp for _, g, _, sp in mm) == _cdiv(N, bmw) * _cdiv(M, bn)
+        # The matmul's launch (with a tail or not) covers its tiles once.
+        _check_step(1, mm, N, K, M)
     else:
         assert len(mm) == 1 and M <= 8
     assert smm.workspace_size(M, K, N) >= M * K * 2 + M * 4
